@@ -1,0 +1,198 @@
+#!/usr/bin/env python3
+"""Throughput of the GBLA forward pass on one MI355X.
+
+A step is one gbla_forward call (Conv1D, key gating, global state, readout
+and gated RMSNorm of every head) over one batch of synthetic inputs already
+resident in HBM.  Default workload: B=1, H=8, n=32768, d=64, bf16 inputs,
+conv width 4.  Several copies of the inputs and outputs (at least 1 GiB in
+total) are used round-robin so the 256 MB last-level cache cannot hold a
+step's working set.
+
+Prints one JSON line (rank 0) with the metric, the roofline of the dominant
+kernel (timed live with HIP events on the launch stream) and the fp64 oracle
+timed on the host cores over a bounded sample.
+"""
+import argparse
+import hashlib
+import json
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "GBLA fwd tokens/sec at n=32768,H=8,d=64; % of HBM roofline (rocprof)"
+HBM_PEAK_GBPS = 8000.0
+PROFILES = os.path.join(ROOT, "profiles")
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for f in ("gbla_kernels.hip", "gbla_api.cpp", "gbla_plan.h"):
+        with open(os.path.join(ROOT, "paper_2606_07317_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def algorithmic_bytes(inp, part: str) -> int:
+    """Bytes each stage must move at least once (inputs read once, y written once).
+    Per token and head, with e = element size of the inputs:
+      state:   k, v (2 d e) + a (e)          = (2d + 1) e
+      readout: q, r (2 d e) + y (4 d)        = 2 d e + 4 d
+      forward: (4d + 1) e + 4 d               (770 B at d = 64, bf16)"""
+    w = inp.workload
+    e = 2 if w.dtype == "bf16" else 4
+    d = w.head_dim
+    th = inp.tokens * w.heads
+    per = {"state": (2 * d + 1) * e, "readout": 2 * d * e + 4 * d,
+           "forward": (4 * d + 1) * e + 4 * d}[part]
+    return th * per
+
+
+def traffic_from_profiles(kernel: str, workload: str):
+    """HBM bytes per launch measured with rocprofv3 counters, if the committed
+    measurement was taken on the current kernel sources."""
+    path = os.path.join(PROFILES, "traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        rec = json.load(open(path)).get("%s/%s" % (kernel, workload))
+    except (ValueError, OSError):
+        return None
+    if not rec or rec.get("source_hash") != kernel_source_hash():
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def cpu_baseline(inp, seconds: float):
+    import oracle
+    orc = oracle.load()
+    threads = orc.max_threads()
+    units = inp.nseq * inp.workload.heads
+    times = []
+    t_start = time.perf_counter()
+    while True:
+        t0 = time.perf_counter()
+        orc.forward_inputs(inp, want=("y",), nthreads=threads)
+        times.append(time.perf_counter() - t0)
+        if len(times) >= 3 and time.perf_counter() - t_start >= seconds:
+            break
+        if len(times) >= 50:
+            break
+    med = statistics.median(times)
+    return {"value": inp.tokens / med, "unit": "tokens/s", "cores": min(threads, units),
+            "kind": "oracle",
+            "sample": "the full %s batch (%d tokens x %d heads), fp64, %d runs, median %.3f s"
+                      % (inp.workload.name, inp.tokens, inp.workload.heads, len(times), med)}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=400)
+    ap.add_argument("--warmup", type=int, default=40)
+    ap.add_argument("--workload", default=None)
+    ap.add_argument("--sets", type=int, default=0, help="rotated input sets (0: enough for 1 GiB)")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2606_07317_amd import gbla, inputs
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    dev = torch.device("cuda:0")
+    wname = args.workload or inputs.THROUGHPUT_WORKLOAD
+    inp = inputs.make_inputs(wname)
+    w = inp.workload
+    base = inputs.device_tensors(inp, dev)
+    per_set = sum(base[n].numel() * base[n].element_size() for n in ("q", "k", "v", "a", "r"))
+    per_set += base["q"].numel() * 4
+    nsets = args.sets or max(2, -(-(1 << 30) // per_set) + 1)
+    sets = []
+    for i in range(nsets):
+        t = {n: (base[n].clone() if isinstance(base[n], torch.Tensor) else base[n]) for n in base}
+        t["out"] = torch.empty(base["q"].shape, dtype=torch.float32, device=dev)
+        sets.append(t)
+    shape = gbla.make_shape(base["q"], base["conv_w"], inp.eps, base["cu_seqlens"], base["max_seqlen"])
+    ws = gbla.alloc_workspace(shape, dev)
+
+    def step(i):
+        t = sets[i % nsets]
+        gbla.forward(t["q"], t["k"], t["v"], t["a"], t["r"], t["conv_w"], t["gamma"], eps=inp.eps,
+                     cu_seqlens=t["cu_seqlens"], max_seqlen=t["max_seqlen"], workspace=ws,
+                     out=t["out"])
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for i in range(args.steps):
+        step(i)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_per_step = ev0.elapsed_time(ev1) / args.steps
+
+    # Live per-kernel timing of the dominant stage (the readout: 2/3 of the
+    # algorithmic bytes), bracketed by events on the launch stream.
+    n_meas = min(args.steps, 200)
+    pairs = []
+    for i in range(n_meas):
+        t = sets[i % nsets]
+        gbla.state(t["k"], t["v"], t["a"], t["conv_w"], cu_seqlens=t["cu_seqlens"],
+                   max_seqlen=t["max_seqlen"], workspace=ws)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        gbla.readout(t["q"], t["r"], t["conv_w"], t["gamma"], ws, eps=inp.eps,
+                     cu_seqlens=t["cu_seqlens"], max_seqlen=t["max_seqlen"], out=t["out"])
+        b.record(stream)
+        pairs.append((a, b))
+    torch.cuda.synchronize()
+    readout_ms = statistics.mean(a.elapsed_time(b) for a, b in pairs)
+    ach = algorithmic_bytes(inp, "readout") / (readout_ms * 1e-3) / 1e9
+    fwd_gbps = algorithmic_bytes(inp, "forward") / (ms_per_step * 1e-3) / 1e9
+
+    res = {
+        "metric": METRIC,
+        "value": inp.tokens / (ms_per_step * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if w.dtype == "bf16" else "f32",
+        "data": "synthetic",
+        "config": {"workload": w.name, "B": inp.nseq, "H": w.heads, "n": w.seqlen if not w.ragged else None,
+                   "tokens": inp.tokens, "d": w.head_dim, "conv_width": w.conv_width,
+                   "inputs": w.dtype, "output": "f32", "rotating_sets": nsets,
+                   "forward_effective_GBps": round(fwd_gbps, 1),
+                   "forward_hbm_frac": round(fwd_gbps / HBM_PEAK_GBPS, 4),
+                   "wall_s": round(wall, 4)},
+        "roofline": {"bound": "hbm", "kernel": "readout_kernel", "achieved": round(ach, 1),
+                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBPS, 4),
+                     "avg_launch_ms": readout_ms,
+                     "traffic": traffic_from_profiles("readout_kernel", w.name)},
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(inp, args.cpu_seconds)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

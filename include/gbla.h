@@ -1,0 +1,139 @@
+/*
+ * gbla.h -- C ABI of the MI355X (gfx950) GBLA forward pass.
+ *
+ * Gated Bidirectional Linear Attention (Section 2.1 of the paper) over the
+ * projected tensors of every head:
+ *
+ *   qt, kt, vt = causal depthwise Conv1D of q, k, v        (item "Conv1D")
+ *   g          = softmax over the tokens of the sequence of a   (item "Key gating")
+ *   S = sum_j g_j phi(kt_j) vt_j^T,  z = sum_j g_j phi(kt_j)    (its matrix form)
+ *   o_i = phi(qt_i)^T S / phi(qt_i)^T z                          (same display)
+ *   y_i = RmsNorm(o_i) * gamma * SiLU(r_i)                   (item "RMSNorm with gating")
+ *
+ * with phi(x) = elu(x) + 1 (Section 2, Bidirectional Linear Attention
+ * paragraph).  The Conv1D is applied to the projected q, k, v of each head
+ * (depthwise: separate taps per tensor, head and channel; tap W-1 multiplies
+ * the current token; no bias); it does not cross sequence starts.  The key
+ * gate logits a and the output-gate input r are taken as given.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Every array argument is a DEVICE pointer owned by the caller.  The
+ *   library never allocates, frees or synchronizes device memory and keeps
+ *   no mutable global state; calls on different streams are independent as
+ *   long as each stream uses its own workspace.
+ * - Layouts are contiguous, row-major, head_dim fastest:
+ *     dense  (cu_seqlens == NULL): activations [B, H, n, d], logits [B, H, n]
+ *     ragged (cu_seqlens != NULL): activations [H, T, d],    logits [H, T]
+ *   where T = cu_seqlens[N_s] is the packed token count.  In both cases
+ *   shape->seqlen is n (dense) or T (ragged) and shape->batch is B or N_s.
+ * - Base pointers of activations, outputs, weights and the workspace must be
+ *   16-byte aligned (the workspace 256-byte aligned); the logits need only
+ *   their element alignment.  Otherwise GBLA_ERR_MISALIGNED.
+ * - cu_seqlens (int32, device, N_s + 1 entries) is a precondition, not
+ *   checked on the host: cu[0] = 0, non-decreasing, cu[N_s] = T.  Empty
+ *   sequences are allowed (they produce no rows and a zero state).
+ * - All argument checks run on the host before anything is enqueued; on an
+ *   error nothing is launched.  A failed launch returns GBLA_ERR_HIP.
+ *   Device faults surface at the caller's next synchronization.  Nothing is
+ *   thrown across the ABI.  The calls do not synchronize the stream.
+ * - stream is a hipStream_t (NULL = the null stream).
+ */
+#ifndef GBLA_H
+#define GBLA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  GBLA_OK = 0,
+  GBLA_ERR_INVALID_ARGUMENT = 1, /* null pointer, negative size, bad eps     */
+  GBLA_ERR_UNSUPPORTED = 2,      /* head_dim, conv_width or dtype not built   */
+  GBLA_ERR_MISALIGNED = 3,       /* a base pointer breaks the alignment rule  */
+  GBLA_ERR_WORKSPACE = 4,        /* workspace missing or too small            */
+  GBLA_ERR_HIP = 5               /* the HIP runtime reported an error         */
+} gbla_status;
+
+typedef enum { GBLA_F32 = 0, GBLA_BF16 = 1 } gbla_dtype;
+
+typedef struct {
+  int32_t batch;      /* B (dense) or N_s, the number of sequences (ragged)      */
+  int32_t heads;      /* H >= 1                                                  */
+  int32_t seqlen;     /* n (dense) or T = cu_seqlens[N_s] (ragged), >= 0          */
+  int32_t head_dim;   /* d in {32, 64, 128}                                      */
+  int32_t conv_width; /* W in [1, 4]                                             */
+  int32_t max_seqlen; /* ragged: an upper bound of the lengths (>= 0); dense: 0  */
+  int32_t dtype;      /* gbla_dtype of q, k, v, gate_logits and out_gate         */
+  float eps;          /* RMSNorm epsilon, finite and >= 0                        */
+} gbla_shape;
+
+/*
+ * Bytes of device scratch that gbla_forward / gbla_state need for this
+ * shape, for both the dense and the ragged layout.  Pure host arithmetic;
+ * returns 0 for an invalid shape.  The caller allocates it once (any
+ * contents): the entry points initialise what they use on every call.
+ */
+size_t gbla_workspace_bytes(const gbla_shape* shape);
+
+/*
+ * The whole forward pass (Section 2.1: Conv1D, key gating, the global state,
+ * the readout and the gated RMSNorm).
+ *   q, k, v      [B,H,n,d] or [H,T,d], dtype = shape->dtype; pre-conv projections
+ *   gate_logits  [B,H,n]   or [H,T],   dtype = shape->dtype; a = X~ w_g per head
+ *   out_gate     [B,H,n,d] or [H,T,d], dtype = shape->dtype; r = X~ W_R per head
+ *   conv_w       [3,H,d,W] fp32, taps of q, k, v in that order
+ *   norm_w       [H,d] fp32, the RMSNorm weight gamma
+ *   cu_seqlens   NULL (dense) or int32 [N_s + 1] (ragged)
+ *   workspace    >= gbla_workspace_bytes(shape) bytes of device scratch
+ *   out          [B,H,n,d] or [H,T,d] fp32, y
+ */
+gbla_status gbla_forward(const gbla_shape* shape, const void* q, const void* k,
+                         const void* v, const void* gate_logits, const void* out_gate,
+                         const float* conv_w, const float* norm_w,
+                         const int32_t* cu_seqlens, void* workspace,
+                         size_t workspace_bytes, float* out, void* stream);
+
+/*
+ * The Conv1D alone (Section 2.1, item "Conv1D"): writes the convolved
+ * q_t, k_t, v_t (fp32, same layout as q) of every token.  Test hook; the
+ * forward pass fuses the conv into its loads and never writes these.
+ */
+gbla_status gbla_conv1d(const gbla_shape* shape, const void* q, const void* k,
+                        const void* v, const float* conv_w, const int32_t* cu_seqlens,
+                        float* q_t, float* k_t, float* v_t, void* stream);
+
+/*
+ * The global state alone (Section 2.1, key-gating item, matrix form):
+ *   S [N,H,d,d] fp32 with S[c][e] = sum_j g_j phi(kt_j)[c] vt_j[e],
+ *   z [N,H,d]   fp32 with z[c]    = sum_j g_j phi(kt_j)[c],
+ * N = B (dense) or N_s (ragged), g the softmax-normalised gates (sum 1).
+ * Leaves the readout operands in the workspace for gbla_readout.
+ */
+gbla_status gbla_state(const gbla_shape* shape, const void* k, const void* v,
+                       const void* gate_logits, const float* conv_w,
+                       const int32_t* cu_seqlens, void* workspace, size_t workspace_bytes,
+                       float* S, float* z, void* stream);
+
+/*
+ * The readout and gated RMSNorm alone (o_i = phi(qt_i)^T S / phi(qt_i)^T z,
+ * then y), reading the state that the last gbla_state call with the same
+ * shape left in this workspace.  Stage hook for tests and timing; the
+ * result equals gbla_forward's.
+ */
+gbla_status gbla_readout(const gbla_shape* shape, const void* q, const void* out_gate,
+                         const float* conv_w, const float* norm_w,
+                         const int32_t* cu_seqlens, void* workspace,
+                         size_t workspace_bytes, float* out, void* stream);
+
+/* A static, human-readable name of a status code (never NULL). */
+const char* gbla_status_string(gbla_status status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GBLA_H */

@@ -1,0 +1,205 @@
+// gbla_api.cpp -- the C ABI of libgbla.so: argument validation, the launch
+// plan and the entry points declared in include/gbla.h.
+//
+// Every check runs on the host before anything is enqueued, and none of them
+// touches the HIP runtime, so a rejected call has no side effect.
+#include <math.h>
+#include <stdint.h>
+
+#include "gbla.h"
+#include "gbla_plan.h"
+
+namespace gbla {
+namespace {
+
+constexpr int kMaxGridY = 65535;
+constexpr int64_t kMaxGridX = 2147483647LL;
+constexpr int kReadoutTile = 512;
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+int64_t next_pow2(int64_t x) {
+  int64_t p = 1;
+  while (p < x) p <<= 1;
+  return p;
+}
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+}  // namespace
+
+gbla_status make_plan(const gbla_shape* s, bool ragged, Plan* p) {
+  if (!s || !p) return GBLA_ERR_INVALID_ARGUMENT;
+  if (s->batch < 1 || s->heads < 1 || s->seqlen < 0) return GBLA_ERR_INVALID_ARGUMENT;
+  if (s->head_dim != 32 && s->head_dim != 64 && s->head_dim != 128) return GBLA_ERR_UNSUPPORTED;
+  if (s->conv_width < 1 || s->conv_width > 4) return GBLA_ERR_UNSUPPORTED;
+  if (s->dtype != GBLA_F32 && s->dtype != GBLA_BF16) return GBLA_ERR_UNSUPPORTED;
+  if (!(s->eps >= 0.0f) || !isfinite(s->eps)) return GBLA_ERR_INVALID_ARGUMENT;
+  if (ragged && s->max_seqlen < 0) return GBLA_ERR_INVALID_ARGUMENT;
+  if (s->heads > kMaxGridY) return GBLA_ERR_UNSUPPORTED;
+
+  Plan q{};
+  q.nseq = s->batch;
+  q.heads = s->heads;
+  q.rows = s->seqlen;
+  q.d = s->head_dim;
+  q.W = s->conv_width;
+  q.dtype = s->dtype;
+  q.ragged = ragged ? 1 : 0;
+  q.eps = s->eps;
+  q.tokens = ragged ? (int64_t)s->seqlen : (int64_t)s->batch * s->seqlen;
+
+  // Chunk of the state reduction: about one workgroup per CU over all heads,
+  // a power of two between 256 and 2048 tokens.  Depends on the shape only.
+  const int64_t work = q.tokens * q.heads;
+  int64_t chunk = next_pow2((work + 255) / 256);
+  if (chunk < 256) chunk = 256;
+  if (chunk > 2048) chunk = 2048;
+  q.chunk = (int32_t)chunk;
+  q.rtile = kReadoutTile;
+
+  // Upper bounds valid for both layouts: sum_s max(1, ceil(len_s / u)) <=
+  // tokens / u + N.  The partial records are sized with this bound so the
+  // workspace layout is the same for the dense and the ragged call.
+  const int64_t units_cap = q.tokens / q.chunk + q.nseq;
+  const int64_t runits_cap = q.tokens / q.rtile + q.nseq;
+  if (units_cap > kMaxGridX || runits_cap > kMaxGridX) return GBLA_ERR_UNSUPPORTED;
+  if (ragged) {
+    q.chunks_per_seq = 0;
+    q.rtiles_per_seq = 0;
+    q.units = (int32_t)units_cap;
+    q.runits = (int32_t)runits_cap;
+  } else {
+    int64_t cps = ((int64_t)q.rows + q.chunk - 1) / q.chunk;
+    int64_t rps = ((int64_t)q.rows + q.rtile - 1) / q.rtile;
+    if (cps < 1) cps = 1;
+    if (rps < 1) rps = 1;
+    q.chunks_per_seq = (int32_t)cps;
+    q.rtiles_per_seq = (int32_t)rps;
+    q.units = (int32_t)(cps * q.nseq);
+    q.runits = (int32_t)(rps * q.nseq);
+  }
+
+  q.rec_floats = (int32_t)align_up((size_t)q.d * q.d + q.d + 2, 64);
+  const size_t nmb = q.d / 16 + 1, nkb = q.d / 32;
+  const size_t lane_bytes = q.dtype == GBLA_BF16 ? 16 : 32;
+  q.frag_bytes = align_up(nmb * nkb * 64 * lane_bytes, 256);
+  q.off_partials = 0;
+  const size_t part_bytes = (size_t)units_cap * q.heads * q.rec_floats * sizeof(float);
+  q.off_frags = align_up(q.off_partials + part_bytes, 256);
+  q.total_bytes = align_up(q.off_frags + (size_t)q.nseq * q.heads * q.frag_bytes, 256);
+  *p = q;
+  return GBLA_OK;
+}
+
+}  // namespace gbla
+
+using gbla::Plan;
+
+namespace {
+
+gbla_status check_ws(const Plan& p, const void* ws, size_t ws_bytes) {
+  if (!ws) return GBLA_ERR_WORKSPACE;
+  if (!gbla::aligned(ws, 256)) return GBLA_ERR_MISALIGNED;
+  if (ws_bytes < p.total_bytes) return GBLA_ERR_WORKSPACE;
+  return GBLA_OK;
+}
+
+size_t elem_bytes(const Plan& p) { return p.dtype == GBLA_BF16 ? 2 : 4; }
+
+gbla_status check_acts(const Plan& p, std::initializer_list<const void*> acts) {
+  for (const void* a : acts) {
+    if (!a) return GBLA_ERR_INVALID_ARGUMENT;
+    if (!gbla::aligned(a, 16)) return GBLA_ERR_MISALIGNED;
+  }
+  (void)p;
+  return GBLA_OK;
+}
+
+gbla_status check_logits(const Plan& p, const void* a) {
+  if (!a) return GBLA_ERR_INVALID_ARGUMENT;
+  if (!gbla::aligned(a, elem_bytes(p))) return GBLA_ERR_MISALIGNED;
+  return GBLA_OK;
+}
+
+#define GBLA_TRY(expr)                  \
+  do {                                  \
+    gbla_status _st = (expr);           \
+    if (_st != GBLA_OK) return _st;     \
+  } while (0)
+
+}  // namespace
+
+extern "C" {
+
+size_t gbla_workspace_bytes(const gbla_shape* shape) {
+  // The shape alone does not say whether cu_seqlens will be given, so the
+  // size covers both readings (dense: B*n tokens, ragged: T = seqlen tokens).
+  Plan dense, ragged;
+  if (gbla::make_plan(shape, false, &dense) != GBLA_OK) return 0;
+  if (gbla::make_plan(shape, true, &ragged) != GBLA_OK) return 0;
+  return dense.total_bytes > ragged.total_bytes ? dense.total_bytes : ragged.total_bytes;
+}
+
+gbla_status gbla_forward(const gbla_shape* shape, const void* q, const void* k, const void* v,
+                         const void* gate_logits, const void* out_gate, const float* conv_w,
+                         const float* norm_w, const int32_t* cu_seqlens, void* workspace,
+                         size_t workspace_bytes, float* out, void* stream) {
+  Plan p;
+  GBLA_TRY(gbla::make_plan(shape, cu_seqlens != nullptr, &p));
+  GBLA_TRY(check_acts(p, {q, k, v, out_gate, conv_w, norm_w, out}));
+  GBLA_TRY(check_logits(p, gate_logits));
+  GBLA_TRY(check_ws(p, workspace, workspace_bytes));
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  GBLA_TRY(gbla::launch_state(p, k, v, gate_logits, conv_w, cu_seqlens, workspace, nullptr,
+                              nullptr, st));
+  return gbla::launch_readout(p, q, out_gate, conv_w, norm_w, cu_seqlens, workspace, out, st);
+}
+
+gbla_status gbla_conv1d(const gbla_shape* shape, const void* q, const void* k, const void* v,
+                        const float* conv_w, const int32_t* cu_seqlens, float* q_t, float* k_t,
+                        float* v_t, void* stream) {
+  Plan p;
+  GBLA_TRY(gbla::make_plan(shape, cu_seqlens != nullptr, &p));
+  GBLA_TRY(check_acts(p, {q, k, v, conv_w, q_t, k_t, v_t}));
+  return gbla::launch_conv(p, q, k, v, conv_w, cu_seqlens, q_t, k_t, v_t,
+                           static_cast<hipStream_t>(stream));
+}
+
+gbla_status gbla_state(const gbla_shape* shape, const void* k, const void* v,
+                       const void* gate_logits, const float* conv_w, const int32_t* cu_seqlens,
+                       void* workspace, size_t workspace_bytes, float* S, float* z,
+                       void* stream) {
+  Plan p;
+  GBLA_TRY(gbla::make_plan(shape, cu_seqlens != nullptr, &p));
+  GBLA_TRY(check_acts(p, {k, v, conv_w, S, z}));
+  GBLA_TRY(check_logits(p, gate_logits));
+  GBLA_TRY(check_ws(p, workspace, workspace_bytes));
+  return gbla::launch_state(p, k, v, gate_logits, conv_w, cu_seqlens, workspace, S, z,
+                            static_cast<hipStream_t>(stream));
+}
+
+gbla_status gbla_readout(const gbla_shape* shape, const void* q, const void* out_gate,
+                         const float* conv_w, const float* norm_w, const int32_t* cu_seqlens,
+                         void* workspace, size_t workspace_bytes, float* out, void* stream) {
+  Plan p;
+  GBLA_TRY(gbla::make_plan(shape, cu_seqlens != nullptr, &p));
+  GBLA_TRY(check_acts(p, {q, out_gate, conv_w, norm_w, out}));
+  GBLA_TRY(check_ws(p, workspace, workspace_bytes));
+  return gbla::launch_readout(p, q, out_gate, conv_w, norm_w, cu_seqlens, workspace, out,
+                              static_cast<hipStream_t>(stream));
+}
+
+const char* gbla_status_string(gbla_status status) {
+  switch (status) {
+    case GBLA_OK: return "GBLA_OK";
+    case GBLA_ERR_INVALID_ARGUMENT: return "GBLA_ERR_INVALID_ARGUMENT";
+    case GBLA_ERR_UNSUPPORTED: return "GBLA_ERR_UNSUPPORTED";
+    case GBLA_ERR_MISALIGNED: return "GBLA_ERR_MISALIGNED";
+    case GBLA_ERR_WORKSPACE: return "GBLA_ERR_WORKSPACE";
+    case GBLA_ERR_HIP: return "GBLA_ERR_HIP";
+  }
+  return "GBLA_ERR_UNKNOWN";
+}
+
+}  // extern "C"

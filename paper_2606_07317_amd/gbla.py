@@ -1,0 +1,226 @@
+"""Python binding of libgbla.so (argument marshalling only).
+
+Every step of the GBLA forward pass runs in the HIP kernels behind the C ABI
+declared in ``include/gbla.h``; this module checks tensor metadata, passes
+device pointers and the current HIP stream, and turns status codes into
+exceptions.  PyTorch provides device memory and streams, nothing else.  If
+the library is not built this module raises; there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+from typing import Optional, Tuple
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libgbla.so")
+HEADER_PATH = os.path.join(os.path.dirname(_PKG), "include", "gbla.h")
+
+GBLA_F32 = 0
+GBLA_BF16 = 1
+STATUS_NAMES = {0: "GBLA_OK", 1: "GBLA_ERR_INVALID_ARGUMENT", 2: "GBLA_ERR_UNSUPPORTED",
+                3: "GBLA_ERR_MISALIGNED", 4: "GBLA_ERR_WORKSPACE", 5: "GBLA_ERR_HIP"}
+
+
+class GblaError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__("%s failed: %s" % (where, STATUS_NAMES.get(status, status)))
+
+
+class Shape(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("heads", ctypes.c_int32), ("seqlen", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("conv_width", ctypes.c_int32),
+                ("max_seqlen", ctypes.c_int32), ("dtype", ctypes.c_int32), ("eps", ctypes.c_float)]
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH):
+    """Load libgbla.so and declare its signatures.  Raises if it is missing."""
+    global _lib
+    if _lib is not None and path == LIB_PATH:
+        return _lib
+    if not os.path.exists(path):
+        raise GblaError(-1, "loading %s (not built: run __graft_entry__.build())" % path)
+    lib = ctypes.CDLL(path)
+    P = ctypes.c_void_p
+    SP = ctypes.POINTER(Shape)
+    sz = ctypes.c_size_t
+    lib.gbla_workspace_bytes.argtypes = [SP]
+    lib.gbla_workspace_bytes.restype = sz
+    lib.gbla_forward.argtypes = [SP, P, P, P, P, P, P, P, P, P, sz, P, P]
+    lib.gbla_forward.restype = ctypes.c_int
+    lib.gbla_conv1d.argtypes = [SP, P, P, P, P, P, P, P, P, P]
+    lib.gbla_conv1d.restype = ctypes.c_int
+    lib.gbla_state.argtypes = [SP, P, P, P, P, P, P, sz, P, P, P]
+    lib.gbla_state.restype = ctypes.c_int
+    lib.gbla_readout.argtypes = [SP, P, P, P, P, P, P, sz, P, P]
+    lib.gbla_readout.restype = ctypes.c_int
+    lib.gbla_status_string.argtypes = [ctypes.c_int]
+    lib.gbla_status_string.restype = ctypes.c_char_p
+    if path == LIB_PATH:
+        _lib = lib
+    return lib
+
+
+def declared_functions(header: str = HEADER_PATH):
+    """Names of the functions that include/gbla.h declares."""
+    text = open(header).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(gbla_[a-z0-9_]+)\s*\(", text)))
+
+
+# ---------------------------------------------------------------------------
+# Tensor marshalling.
+# ---------------------------------------------------------------------------
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return GBLA_BF16
+    if t.dtype == torch.float32:
+        return GBLA_F32
+    raise TypeError("activations must be bfloat16 or float32, got %s" % t.dtype)
+
+
+def _check(t: torch.Tensor, name: str, dtype=None, device=None):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError("%s must be a torch.Tensor" % name)
+    if not t.is_cuda:
+        raise ValueError("%s must live on the GPU" % name)
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError("%s must be %s, got %s" % (name, dtype, t.dtype))
+    if device is not None and t.device != device:
+        raise ValueError("%s is on %s, expected %s" % (name, t.device, device))
+
+
+def make_shape(q: torch.Tensor, conv_w: torch.Tensor, eps: float,
+               cu_seqlens: Optional[torch.Tensor], max_seqlen: Optional[int]) -> Shape:
+    if cu_seqlens is None:
+        if q.dim() != 4:
+            raise ValueError("dense q must be [B, H, n, d]")
+        B, H, n, d = q.shape
+        batch, rows, msl = B, n, 0
+    else:
+        if q.dim() != 3:
+            raise ValueError("ragged q must be [H, T, d]")
+        H, rows, d = q.shape
+        batch = cu_seqlens.numel() - 1
+        msl = int(max_seqlen) if max_seqlen is not None else rows
+    if conv_w.dim() != 4 or tuple(conv_w.shape[:3]) != (3, H, d):
+        raise ValueError("conv_w must be [3, H, d, W]")
+    return Shape(batch, H, rows, d, conv_w.shape[3], msl, _dtype_code(q), float(eps))
+
+
+def _stream(stream) -> int:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _raise(st: int, where: str):
+    if st != 0:
+        raise GblaError(st, where)
+
+
+def workspace_bytes(shape: Shape) -> int:
+    n = load_library().gbla_workspace_bytes(ctypes.byref(shape))
+    if n == 0:
+        raise GblaError(1, "gbla_workspace_bytes")
+    return int(n)
+
+
+def alloc_workspace(shape: Shape, device) -> torch.Tensor:
+    """Caller-owned scratch for gbla_forward / gbla_state (256-byte aligned)."""
+    return torch.empty(workspace_bytes(shape), dtype=torch.uint8, device=device)
+
+
+def _check_inputs(q, k, v, a, r, conv_w, norm_w, cu_seqlens):
+    dev = q.device
+    for t, nm in ((q, "q"), (k, "k"), (v, "v"), (r, "out_gate")):
+        if t is not None:
+            _check(t, nm, q.dtype, dev)
+            if t.shape != q.shape:
+                raise ValueError("%s has shape %s, expected %s" % (nm, tuple(t.shape), tuple(q.shape)))
+    if a is not None:
+        _check(a, "gate_logits", q.dtype, dev)
+        if a.shape != q.shape[:-1]:
+            raise ValueError("gate_logits must have shape %s" % (tuple(q.shape[:-1]),))
+    _check(conv_w, "conv_w", torch.float32, dev)
+    if norm_w is not None:
+        _check(norm_w, "norm_w", torch.float32, dev)
+        if norm_w.shape != (q.shape[-3], q.shape[-1]):
+            raise ValueError("norm_w must be [H, d]")
+    if cu_seqlens is not None:
+        _check(cu_seqlens, "cu_seqlens", torch.int32, dev)
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else t.data_ptr()
+
+
+def forward(q, k, v, gate_logits, out_gate, conv_w, norm_w, eps: float = 1e-6,
+            cu_seqlens=None, max_seqlen=None, workspace=None, out=None, stream=None) -> torch.Tensor:
+    """y = GBLA(q, k, v, a, r) on the GPU; see include/gbla.h for the layouts."""
+    _check_inputs(q, k, v, gate_logits, out_gate, conv_w, norm_w, cu_seqlens)
+    shape = make_shape(q, conv_w, eps, cu_seqlens, max_seqlen)
+    if workspace is None:
+        workspace = alloc_workspace(shape, q.device)
+    if out is None:
+        out = torch.empty(q.shape, dtype=torch.float32, device=q.device)
+    _check(out, "out", torch.float32, q.device)
+    st = load_library().gbla_forward(
+        ctypes.byref(shape), _ptr(q), _ptr(k), _ptr(v), _ptr(gate_logits), _ptr(out_gate),
+        _ptr(conv_w), _ptr(norm_w), _ptr(cu_seqlens), _ptr(workspace), workspace.numel(),
+        _ptr(out), _stream(stream))
+    _raise(st, "gbla_forward")
+    return out
+
+
+def conv1d(q, k, v, conv_w, cu_seqlens=None, max_seqlen=None, stream=None
+           ) -> Tuple[torch.Tensor, torch.Tensor, torch.Tensor]:
+    """The Conv1D alone: fp32 q_t, k_t, v_t in the layout of q."""
+    _check_inputs(q, k, v, None, None, conv_w, None, cu_seqlens)
+    shape = make_shape(q, conv_w, 0.0, cu_seqlens, max_seqlen)
+    outs = [torch.empty(q.shape, dtype=torch.float32, device=q.device) for _ in range(3)]
+    st = load_library().gbla_conv1d(ctypes.byref(shape), _ptr(q), _ptr(k), _ptr(v), _ptr(conv_w),
+                                    _ptr(cu_seqlens), *[_ptr(o) for o in outs], _stream(stream))
+    _raise(st, "gbla_conv1d")
+    return tuple(outs)
+
+
+def state(k, v, gate_logits, conv_w, cu_seqlens=None, max_seqlen=None, workspace=None,
+          stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """The normalised global state S [N,H,d,d] and z [N,H,d] (fp32)."""
+    _check_inputs(k, k, v, gate_logits, None, conv_w, None, cu_seqlens)
+    shape = make_shape(k, conv_w, 0.0, cu_seqlens, max_seqlen)
+    if workspace is None:
+        workspace = alloc_workspace(shape, k.device)
+    N, H, d = shape.batch, shape.heads, shape.head_dim
+    S = torch.empty((N, H, d, d), dtype=torch.float32, device=k.device)
+    z = torch.empty((N, H, d), dtype=torch.float32, device=k.device)
+    st = load_library().gbla_state(ctypes.byref(shape), _ptr(k), _ptr(v), _ptr(gate_logits),
+                                   _ptr(conv_w), _ptr(cu_seqlens), _ptr(workspace),
+                                   workspace.numel(), _ptr(S), _ptr(z), _stream(stream))
+    _raise(st, "gbla_state")
+    return S, z
+
+
+def readout(q, out_gate, conv_w, norm_w, workspace, eps: float = 1e-6, cu_seqlens=None,
+            max_seqlen=None, out=None, stream=None) -> torch.Tensor:
+    """Readout + gated RMSNorm from the state a preceding state() call left in
+    ``workspace``."""
+    _check_inputs(q, None, None, None, out_gate, conv_w, norm_w, cu_seqlens)
+    shape = make_shape(q, conv_w, eps, cu_seqlens, max_seqlen)
+    if out is None:
+        out = torch.empty(q.shape, dtype=torch.float32, device=q.device)
+    st = load_library().gbla_readout(ctypes.byref(shape), _ptr(q), _ptr(out_gate), _ptr(conv_w),
+                                     _ptr(norm_w), _ptr(cu_seqlens), _ptr(workspace),
+                                     workspace.numel(), _ptr(out), _stream(stream))
+    _raise(st, "gbla_readout")
+    return out

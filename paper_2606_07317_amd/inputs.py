@@ -183,3 +183,27 @@ def to_f64(x: np.ndarray, dtype: str) -> np.ndarray:
     if dtype == BF16:
         return bf16_bits_to_f32(x).astype(np.float64)
     return np.asarray(x, dtype=np.float32).astype(np.float64)
+
+
+def to_torch(x: np.ndarray, dtype: str, device):
+    """Copy one activation array to a torch tensor (bf16 patterns become
+    torch.bfloat16 with the same bits)."""
+    import torch
+    if dtype == BF16:
+        t = torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).view(torch.bfloat16)
+    else:
+        t = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32))
+    return t.to(device)
+
+
+def device_tensors(inp: Inputs, device) -> dict:
+    """All arrays of ``inp`` as torch tensors on ``device``."""
+    import torch
+    dt = inp.workload.dtype
+    out = {n: to_torch(getattr(inp, n), dt, device) for n in ("q", "k", "v", "a", "r")}
+    out["conv_w"] = torch.from_numpy(np.ascontiguousarray(inp.conv_w)).to(device)
+    out["gamma"] = torch.from_numpy(np.ascontiguousarray(inp.gamma)).to(device)
+    out["cu_seqlens"] = (torch.from_numpy(inp.cu_seqlens).to(device)
+                         if inp.cu_seqlens is not None else None)
+    out["max_seqlen"] = int(inp.lengths().max()) if inp.cu_seqlens is not None and inp.nseq else None
+    return out

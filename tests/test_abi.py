@@ -1,0 +1,103 @@
+"""Host-side checks of the C ABI: the library loads, exports every function
+include/gbla.h declares, sizes its workspace from the shape alone, and
+rejects bad arguments before anything reaches the GPU.  No kernel runs here:
+every call below fails validation on the host."""
+import ctypes
+
+import pytest
+
+from paper_2606_07317_amd import gbla
+
+ALIGNED = 0x10000          # fake, 256-byte aligned device addresses; never dereferenced
+MIS = 0x10008
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return gbla.load_library()
+
+
+def shape(**kw):
+    base = dict(batch=1, heads=8, seqlen=32768, head_dim=64, conv_width=4, max_seqlen=0,
+                dtype=gbla.GBLA_BF16, eps=1e-6)
+    base.update(kw)
+    return gbla.Shape(**base)
+
+
+def test_exports_every_declared_function(lib):
+    names = gbla.declared_functions()
+    assert {"gbla_forward", "gbla_workspace_bytes", "gbla_conv1d", "gbla_state",
+            "gbla_readout", "gbla_status_string"} <= set(names)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_status_strings(lib):
+    for code, name in gbla.STATUS_NAMES.items():
+        assert lib.gbla_status_string(code).decode() == name
+    assert lib.gbla_status_string(99).decode() == "GBLA_ERR_UNKNOWN"
+
+
+def test_workspace_bytes(lib):
+    ws = lib.gbla_workspace_bytes(ctypes.byref(shape()))
+    assert ws > 0 and ws % 256 == 0
+    # partial records: at least one (d*d + d + 2)-float record per chunk of every head
+    assert ws >= 8 * 32 * (64 * 64 + 66) * 4
+    # stays modest: under 32 MiB for the n=32768, H=8, d=64 workload
+    assert ws < 32 << 20
+    ragged = lib.gbla_workspace_bytes(ctypes.byref(shape(batch=64, seqlen=190000, head_dim=128,
+                                                         max_seqlen=32768)))
+    assert ragged > 0
+    for bad in (shape(head_dim=48), shape(conv_width=5), shape(conv_width=0), shape(dtype=7),
+                shape(heads=0), shape(batch=0), shape(seqlen=-1), shape(eps=-1.0),
+                shape(eps=float("inf"))):
+        assert lib.gbla_workspace_bytes(ctypes.byref(bad)) == 0
+    assert lib.gbla_workspace_bytes(None) == 0
+
+
+def _forward(lib, s, ws_bytes=None, **ptrs):
+    p = dict(q=ALIGNED, k=ALIGNED, v=ALIGNED, a=ALIGNED, r=ALIGNED, w=ALIGNED, g=ALIGNED,
+             cu=None, ws=ALIGNED, out=ALIGNED)
+    p.update(ptrs)
+    if ws_bytes is None:
+        ws_bytes = lib.gbla_workspace_bytes(ctypes.byref(s))
+    return lib.gbla_forward(ctypes.byref(s), p["q"], p["k"], p["v"], p["a"], p["r"], p["w"], p["g"],
+                            p["cu"], p["ws"], ws_bytes, p["out"], None)
+
+
+def test_forward_rejects_before_launch(lib):
+    s = shape()
+    assert _forward(lib, s, q=None) == 1
+    assert _forward(lib, s, out=None) == 1
+    assert _forward(lib, s, a=None) == 1
+    assert _forward(lib, s, q=MIS) == 3
+    assert _forward(lib, s, out=ALIGNED + 4) == 3
+    assert _forward(lib, s, w=ALIGNED + 4) == 3
+    assert _forward(lib, s, a=ALIGNED + 1) == 3        # bf16 logits need 2-byte alignment
+    assert _forward(lib, s, ws=ALIGNED + 16) == 3      # workspace needs 256 bytes
+    assert _forward(lib, s, ws=None) == 4
+    assert _forward(lib, s, ws_bytes=1024) == 4
+    assert _forward(lib, shape(head_dim=96)) == 2
+    assert _forward(lib, shape(conv_width=8)) == 2
+    assert _forward(lib, shape(dtype=3)) == 2
+    assert _forward(lib, shape(eps=float("nan"))) == 1
+    assert _forward(lib, shape(heads=-2)) == 1
+    assert lib.gbla_forward(None, ALIGNED, ALIGNED, ALIGNED, ALIGNED, ALIGNED, ALIGNED, ALIGNED,
+                            None, ALIGNED, 1 << 30, ALIGNED, None) == 1
+
+
+def test_ragged_requires_nonnegative_bound(lib):
+    s = shape(batch=4, seqlen=100, max_seqlen=-1)
+    assert _forward(lib, s, cu=ALIGNED) == 1
+
+
+def test_other_entry_points_reject_before_launch(lib):
+    s = shape()
+    P = ALIGNED
+    assert lib.gbla_conv1d(ctypes.byref(s), P, P, None, P, None, P, P, P, None) == 1
+    assert lib.gbla_conv1d(ctypes.byref(shape(head_dim=16)), P, P, P, P, None, P, P, P, None) == 2
+    assert lib.gbla_state(ctypes.byref(s), P, P, P, P, None, P, 16, P, P, None) == 4
+    assert lib.gbla_state(ctypes.byref(s), P, P, P, P, None, P + 8, 1 << 40, P, P, None) == 3
+    assert lib.gbla_readout(ctypes.byref(s), None, P, P, P, None, P, 1 << 40, P, None) == 1
+    assert lib.gbla_readout(ctypes.byref(s), P, P, P, P, None, None, 1 << 40, P, None) == 4
+    assert lib.gbla_readout(ctypes.byref(s), P, P, P, P, None, P, 0, P, None) == 4
