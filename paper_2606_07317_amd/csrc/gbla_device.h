@@ -1,0 +1,163 @@
+// gbla_device.h -- device helpers shared by the kernel sources of libgbla.so.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+
+#include "gbla_plan.h"
+
+namespace gbla {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+typedef short i16x4_t __attribute__((ext_vector_type(4)));
+
+constexpr int kThreads = 256;
+
+// bf16 <-> fp32 (bf16 held as raw 16-bit patterns).
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+// Two fp32 -> packed bf16 pair, round to nearest even (v_cvt_pk_bf16_f32).
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  f32x2_t f = {lo, hi};
+  bf16x2_t b = __builtin_convertvector(f, bf16x2_t);
+  return __builtin_bit_cast(uint32_t, b);
+}
+
+__device__ __forceinline__ u32x4_t load16(const void* p) {
+  return *reinterpret_cast<const u32x4_t*>(p);
+}
+
+// Taps of one tensor (0 = q, 1 = k, 2 = v), head h, channel c, right-aligned
+// to four taps: tap 3 multiplies the current token, taps before 4 - W are 0.
+__device__ __forceinline__ void load_taps4(const float* conv_w, int H, int h, int tensor, int D,
+                                           int W, int c, float* w4) {
+  const float* src = conv_w + (((size_t)tensor * H + h) * D + c) * W;
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    const int ti = t - (4 - W);
+    w4[t] = ti >= 0 ? src[ti] : 0.0f;
+  }
+}
+
+__device__ __forceinline__ float wave_max(float x) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) x = fmaxf(x, __shfl_xor(x, o));
+  return x;
+}
+
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o);
+  return x;
+}
+
+__device__ __forceinline__ int wave_incl_scan(int x) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    int y = __shfl_up(x, o);
+    if (lane >= o) x += y;
+  }
+  return x;
+}
+
+__device__ __forceinline__ float block_max(float x, float* red) {
+  x = wave_max(x);
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = x;
+  __syncthreads();
+  return fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+}
+
+// Inclusive scan over the block; *total receives the block sum.
+__device__ __forceinline__ int block_incl_scan(int x, int* red, int* total) {
+  x = wave_incl_scan(x);
+  __syncthreads();
+  if ((threadIdx.x & 63) == 63) red[threadIdx.x >> 6] = x;
+  __syncthreads();
+  const int w = threadIdx.x >> 6;
+  int before = 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) before += i < w ? red[i] : 0;
+  *total = red[0] + red[1] + red[2] + red[3];
+  return x + before;
+}
+
+__device__ __forceinline__ int units_of(int64_t len, int unit) {
+  const int64_t c = (len + unit - 1) / unit;
+  return c < 1 ? 1 : (int)c;
+}
+
+// Ragged batches: find the sequence s and the unit index inside it of the
+// g-th unit of a head, where sequence s owns max(1, ceil(len_s / unit))
+// consecutive units.  Every thread of the block must call it; returns false
+// (for the whole block) when g is past the last unit.
+__device__ __forceinline__ bool locate_unit(const int32_t* cu, int nseq, int unit, int g,
+                                            int* s_out, int* idx_out) {
+  __shared__ int red[4];
+  __shared__ int found[2];
+  if (threadIdx.x == 0) found[0] = -1;
+  int running = 0;
+  for (int base = 0; base < nseq; base += kThreads) {
+    const int s = base + threadIdx.x;
+    int cnt = 0;
+    if (s < nseq) cnt = units_of((int64_t)cu[s + 1] - cu[s], unit);
+    int total;
+    const int incl = block_incl_scan(cnt, red, &total);
+    const int excl = incl - cnt;
+    if (s < nseq && g >= running + excl && g < running + incl) {
+      found[0] = s;
+      found[1] = g - running - excl;
+    }
+    __syncthreads();
+    if (found[0] >= 0) break;
+    running += total;
+  }
+  const int s = found[0];
+  *s_out = s;
+  *idx_out = found[1];
+  return s >= 0;
+}
+
+// Number of units of the sequences before s, summed over the block.
+__device__ __forceinline__ int units_before(const int32_t* cu, int s, int unit) {
+  __shared__ int red[4];
+  int acc = 0;
+  for (int i = threadIdx.x; i < s; i += kThreads) acc += units_of((int64_t)cu[i + 1] - cu[i], unit);
+  int total;
+  (void)block_incl_scan(acc, red, &total);
+  return total;
+}
+
+// Length of sequence s and the row (token index in the [*, rows, d] slice
+// layout) of its token 0 for head h.
+__device__ __forceinline__ void seq_geometry(const Plan& P, const int32_t* cu, int s, int h,
+                                             int64_t* len, int64_t* base_row) {
+  if (P.ragged) {
+    const int64_t c0 = cu[s];
+    *len = (int64_t)cu[s + 1] - c0;
+    *base_row = (int64_t)h * P.rows + c0;
+  } else {
+    *len = P.rows;
+    *base_row = ((int64_t)s * P.heads + h) * P.rows;
+  }
+}
+
+// Find (sequence, unit index) of unit g of a head, dense or ragged.
+__device__ __forceinline__ bool unit_of(const Plan& P, const int32_t* cu, int unit, int per_seq,
+                                        int g, int* s, int* idx) {
+  if (P.ragged) return locate_unit(cu, P.nseq, unit, g, s, idx);
+  *s = g / per_seq;
+  *idx = g - *s * per_seq;
+  return true;
+}
+
+}  // namespace gbla

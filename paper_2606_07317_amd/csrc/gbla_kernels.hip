@@ -31,32 +31,13 @@
 #include <math.h>
 #include <stdint.h>
 
+#include "gbla_device.h"
 #include "gbla_plan.h"
 
 namespace gbla {
 namespace {
 
-typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
-typedef float f32x2_t __attribute__((ext_vector_type(2)));
-typedef float f32x4_t __attribute__((ext_vector_type(4)));
-typedef float f32x16_t __attribute__((ext_vector_type(16)));
-typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
-
-constexpr int kThreads = 256;
 constexpr int kConvRows = 64;  // rows per conv_kernel tile
-
-// ---------------------------------------------------------------------------
-// Element helpers.  T is float (fp32) or uint16_t (bf16 bit patterns).
-// ---------------------------------------------------------------------------
-__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
-__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
-
-__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  f32x2_t f = {lo, hi};
-  bf16x2_t b = __builtin_convertvector(f, bf16x2_t);
-  return __builtin_bit_cast(uint32_t, b);
-}
 
 template <typename T>
 __device__ __forceinline__ float load_scalar(const T* p, int64_t i);
@@ -65,10 +46,6 @@ __device__ __forceinline__ float load_scalar<float>(const float* p, int64_t i) {
 template <>
 __device__ __forceinline__ float load_scalar<uint16_t>(const uint16_t* p, int64_t i) {
   return __uint_as_float((uint32_t)p[i] << 16);
-}
-
-__device__ __forceinline__ u32x4_t load16(const void* p) {
-  return *reinterpret_cast<const u32x4_t*>(p);
 }
 
 // Unpack the 16 bytes at one thread's slot: 8 bf16 or 4 fp32 channels.
@@ -106,119 +83,6 @@ __device__ __forceinline__ float phi(float u) {
 template <typename T>
 __device__ __forceinline__ float silu(float x) {
   return x * __builtin_amdgcn_rcpf(1.0f + gexp<T>(-x));
-}
-
-// Taps of one tensor (0 = q, 1 = k, 2 = v), head h, channel c, right-aligned
-// to four taps: tap 3 multiplies the current token, taps before 4 - W are 0.
-__device__ __forceinline__ void load_taps4(const float* conv_w, int H, int h, int tensor, int D,
-                                           int W, int c, float* w4) {
-  const float* src = conv_w + (((size_t)tensor * H + h) * D + c) * W;
-#pragma unroll
-  for (int t = 0; t < 4; ++t) {
-    const int ti = t - (4 - W);
-    w4[t] = ti >= 0 ? src[ti] : 0.0f;
-  }
-}
-
-// ---------------------------------------------------------------------------
-// Block-wide helpers (256 threads, four wave64s).
-// ---------------------------------------------------------------------------
-__device__ __forceinline__ float wave_max(float x) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) x = fmaxf(x, __shfl_xor(x, o));
-  return x;
-}
-
-__device__ __forceinline__ int wave_incl_scan(int x) {
-  const int lane = threadIdx.x & 63;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    int y = __shfl_up(x, o);
-    if (lane >= o) x += y;
-  }
-  return x;
-}
-
-__device__ float block_max(float x, float* red) {
-  x = wave_max(x);
-  __syncthreads();
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = x;
-  __syncthreads();
-  return fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
-}
-
-// Inclusive scan over the block; *total receives the block sum.
-__device__ int block_incl_scan(int x, int* red, int* total) {
-  x = wave_incl_scan(x);
-  __syncthreads();
-  if ((threadIdx.x & 63) == 63) red[threadIdx.x >> 6] = x;
-  __syncthreads();
-  const int w = threadIdx.x >> 6;
-  int before = 0;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) before += i < w ? red[i] : 0;
-  *total = red[0] + red[1] + red[2] + red[3];
-  return x + before;
-}
-
-__device__ __forceinline__ int units_of(int64_t len, int unit) {
-  const int64_t c = (len + unit - 1) / unit;
-  return c < 1 ? 1 : (int)c;
-}
-
-// Ragged batches: find the sequence s and the chunk index inside it of the
-// g-th unit of a head, where sequence s owns max(1, ceil(len_s / unit))
-// consecutive units.  Every thread of the block must call it; returns false
-// (for the whole block) when g is past the last unit.
-__device__ bool locate_unit(const int32_t* cu, int nseq, int unit, int g, int* s_out,
-                            int* idx_out) {
-  __shared__ int red[4];
-  __shared__ int found[2];
-  if (threadIdx.x == 0) found[0] = -1;
-  int running = 0;
-  for (int base = 0; base < nseq; base += kThreads) {
-    const int s = base + threadIdx.x;
-    int cnt = 0;
-    if (s < nseq) cnt = units_of((int64_t)cu[s + 1] - cu[s], unit);
-    int total;
-    const int incl = block_incl_scan(cnt, red, &total);
-    const int excl = incl - cnt;
-    if (s < nseq && g >= running + excl && g < running + incl) {
-      found[0] = s;
-      found[1] = g - running - excl;
-    }
-    __syncthreads();
-    if (found[0] >= 0) break;
-    running += total;
-  }
-  const int s = found[0];
-  *s_out = s;
-  *idx_out = found[1];
-  return s >= 0;
-}
-
-// Number of units of the sequences before s, summed over the block.
-__device__ int units_before(const int32_t* cu, int s, int unit) {
-  __shared__ int red[4];
-  int acc = 0;
-  for (int i = threadIdx.x; i < s; i += kThreads) acc += units_of((int64_t)cu[i + 1] - cu[i], unit);
-  int total;
-  (void)block_incl_scan(acc, red, &total);
-  return total;
-}
-
-// Length of sequence s and the row (token index of the [*, rows, d] slice
-// layout) of its token 0 for head h.
-__device__ __forceinline__ void seq_geometry(const Plan& P, const int32_t* cu, int s, int h,
-                                             int64_t* len, int64_t* base_row) {
-  if (P.ragged) {
-    const int64_t c0 = cu[s];
-    *len = (int64_t)cu[s + 1] - c0;
-    *base_row = (int64_t)h * P.rows + c0;
-  } else {
-    *len = P.rows;
-    *base_row = ((int64_t)s * P.heads + h) * P.rows;
-  }
 }
 
 // ---------------------------------------------------------------------------
@@ -559,16 +423,21 @@ __device__ __forceinline__ void frag_put(void* frag_sh, int mb, int kb, int lane
   }
 }
 
+// grid = (N * H, element slices of 64).  Thread (x, pg) of a block sums the
+// element x of partials pg, pg + 4, ... (in that order) scaled by
+// exp(m_p - M); the four sums are added in the order pg = 0..3, then divided
+// by Z = sum_p exp(m_p - M) l_p.  The split of the partials is a function of
+// the shape only, so the result is the same on every call.
 template <typename T, int D>
 __global__ void __launch_bounds__(kThreads)
 combine_kernel(Plan P, const int32_t* __restrict__ cu, const float* __restrict__ partials,
                float* __restrict__ S_out, float* __restrict__ z_out, unsigned char* __restrict__ frags) {
   constexpr int kElems = D * D + D;
-  constexpr int kPerThread = 4;
-  __shared__ float coef[kThreads];
   __shared__ float red[4];
-  const int s = blockIdx.x, h = blockIdx.y;
+  __shared__ float part[4][64];
   const int tid = threadIdx.x;
+  const int sh_idx = blockIdx.x;
+  const int s = sh_idx / P.heads, h = sh_idx % P.heads;
   int first, count;
   if (P.ragged) {
     first = units_before(cu, s, P.chunk);
@@ -578,62 +447,50 @@ combine_kernel(Plan P, const int32_t* __restrict__ cu, const float* __restrict__
     count = P.chunks_per_seq;
   }
   const float* recs = partials + ((size_t)h * P.units + first) * P.rec_floats;
-
-  // M = max_p m_p and Z = sum_p exp(m_p - M) l_p, each in a fixed order.
   float mloc = -INFINITY;
   for (int p = tid; p < count; p += kThreads) mloc = fmaxf(mloc, recs[(size_t)p * P.rec_floats + kElems]);
   const float M = block_max(mloc, red);
-  float Z = 0.0f;
-  if (M != -INFINITY) {
-    for (int p = 0; p < count; ++p) {
+  float zl = 0.0f;
+  if (M != -INFINITY)
+    for (int p = tid; p < count; p += kThreads) {
       const float* r = recs + (size_t)p * P.rec_floats + kElems;
-      Z += gexp<T>(r[0] - M) * r[1];
+      zl += gexp<T>(r[0] - M) * r[1];
     }
-  }
+  zl = wave_sum(zl);
+  __syncthreads();
+  if ((tid & 63) == 0) red[tid >> 6] = zl;
+  __syncthreads();
+  const float Z = (red[0] + red[1]) + (red[2] + red[3]);
   const float invZ = Z > 0.0f ? 1.0f / Z : 0.0f;
 
-  float val[kPerThread];
-  int xs[kPerThread];
-#pragma unroll
-  for (int i = 0; i < kPerThread; ++i) {
-    xs[i] = (blockIdx.z * kPerThread + i) * kThreads + tid;
-    val[i] = 0.0f;
-  }
-  for (int pb = 0; pb < count; pb += kThreads) {
-    __syncthreads();
-    if (pb + tid < count) {
-      const float mp = recs[(size_t)(pb + tid) * P.rec_floats + kElems];
-      coef[tid] = invZ > 0.0f ? gexp<T>(mp - M) * invZ : 0.0f;
-    }
-    __syncthreads();
-    const int n = min(kThreads, count - pb);
-    for (int p = 0; p < n; ++p) {
-      const float cp = coef[p];
-      const float* r = recs + (size_t)(pb + p) * P.rec_floats;
-#pragma unroll
-      for (int i = 0; i < kPerThread; ++i)
-        if (xs[i] < kElems) val[i] = fmaf(cp, r[xs[i]], val[i]);
+  const int xl = tid & 63, pg = tid >> 6;
+  const int x = blockIdx.y * 64 + xl;
+  float v = 0.0f;
+  if (x < kElems && invZ > 0.0f) {
+#pragma unroll 4
+    for (int p = pg; p < count; p += 4) {
+      const float* r = recs + (size_t)p * P.rec_floats;
+      v = fmaf(gexp<T>(r[kElems] - M), r[x], v);
     }
   }
+  part[pg][xl] = v;
+  __syncthreads();
+  if (tid >= 64 || x >= kElems) return;
+  const float val = (((part[0][xl] + part[1][xl]) + part[2][xl]) + part[3][xl]) * invZ;
 
   const size_t sh = (size_t)s * P.heads + h;
   unsigned char* fr = frags + sh * P.frag_bytes;
-#pragma unroll
-  for (int i = 0; i < kPerThread; ++i) {
-    const int x = xs[i];
-    if (x >= kElems) continue;
-    if (x < D * D) {
-      const int c = x / D, e = x % D;
-      if (S_out) S_out[sh * D * D + x] = val[i];
-      const int kb = c / 32, gq = (c % 32) / 8, j = c % 8;
-      const int mb = 2 * (e / 32) + (e % 8) / 4, m = 4 * ((e % 32) / 8) + e % 4;
-      frag_put<T, D>(fr, mb, kb, 16 * gq + m, j, val[i]);
-    } else {
-      const int c = x - D * D;
-      if (z_out) z_out[sh * D + c] = val[i];
-      const int kb = c / 32, gq = (c % 32) / 8, j = c % 8;
-      for (int m = 0; m < 16; ++m) frag_put<T, D>(fr, D / 16, kb, 16 * gq + m, j, val[i]);
-    }
+  if (x < D * D) {
+    const int c = x / D, e = x % D;
+    if (S_out) S_out[sh * D * D + x] = val;
+    const int kb = c / 32, gq = (c % 32) / 8, j = c % 8;
+    const int mb = 2 * (e / 32) + (e % 8) / 4, m = 4 * ((e % 32) / 8) + e % 4;
+    frag_put<T, D>(fr, mb, kb, 16 * gq + m, j, val);
+  } else {
+    const int c = x - D * D;
+    if (z_out) z_out[sh * D + c] = val;
+    const int kb = c / 32, gq = (c % 32) / 8, j = c % 8;
+    for (int m = 0; m < 16; ++m) frag_put<T, D>(fr, D / 16, kb, 16 * gq + m, j, val);
   }
 }
 
@@ -909,14 +766,19 @@ struct StateRun {
                          hipStream_t st) {
     unsigned char* base = static_cast<unsigned char*>(ws);
     float* partials = reinterpret_cast<float*>(base + p.off_partials);
-    hipLaunchKernelGGL((state_partial_kernel<T, D>), dim3(p.units, p.heads), dim3(kThreads), 0, st,
-                       p, (const T*)k, (const T*)v, (const T*)a, w, cu, partials);
-    gbla_status e = last_launch_status();
+    gbla_status e;
+    if (stream_supported(p)) {
+      e = launch_state_stream(p, k, v, a, w, cu, partials, st);
+    } else {
+      hipLaunchKernelGGL((state_partial_kernel<T, D>), dim3(p.units, p.heads), dim3(kThreads), 0,
+                         st, p, (const T*)k, (const T*)v, (const T*)a, w, cu, partials);
+      e = last_launch_status();
+    }
     if (e != GBLA_OK) return e;
     constexpr int kElems = D * D + D;
-    const int blocks = (kElems + 4 * kThreads - 1) / (4 * kThreads);
-    hipLaunchKernelGGL((combine_kernel<T, D>), dim3(p.nseq, p.heads, blocks), dim3(kThreads), 0, st,
-                       p, cu, (const float*)partials, S, z, base + p.off_frags);
+    const int slices = (kElems + 63) / 64;
+    hipLaunchKernelGGL((combine_kernel<T, D>), dim3(p.nseq * p.heads, slices), dim3(kThreads), 0,
+                       st, p, cu, (const float*)partials, S, z, base + p.off_frags);
     return last_launch_status();
   }
 };
@@ -928,6 +790,8 @@ struct ReadoutRun {
                          hipStream_t st) {
     if (p.tokens == 0) return GBLA_OK;
     const unsigned char* base = static_cast<const unsigned char*>(ws);
+    if (stream_supported(p))
+      return launch_readout_stream(p, q, r, w, gamma, cu, base + p.off_frags, out, st);
     hipLaunchKernelGGL((readout_kernel<T, D>), dim3(p.runits, p.heads), dim3(kThreads), 0, st,
                        p, (const T*)q, (const T*)r, w, gamma, cu, base + p.off_frags, out);
     return last_launch_status();

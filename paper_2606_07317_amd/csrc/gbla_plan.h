@@ -60,4 +60,13 @@ gbla_status launch_readout(const Plan& p, const void* q, const void* r, const fl
                            const float* gamma, const int32_t* cu, const void* workspace,
                            float* out, hipStream_t stream);
 
+// Streaming kernels (gbla_stream.hip): bf16 inputs, head dim 32 or 64.
+bool stream_supported(const Plan& p);
+gbla_status launch_state_stream(const Plan& p, const void* k, const void* v, const void* a,
+                                const float* conv_w, const int32_t* cu, float* partials,
+                                hipStream_t stream);
+gbla_status launch_readout_stream(const Plan& p, const void* q, const void* r, const float* conv_w,
+                                  const float* gamma, const int32_t* cu, const unsigned char* frags,
+                                  float* out, hipStream_t stream);
+
 }  // namespace gbla
