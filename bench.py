@@ -30,7 +30,7 @@ PROFILES = os.path.join(ROOT, "profiles")
 
 def kernel_source_hash() -> str:
     h = hashlib.sha256()
-    for f in ("gbla_kernels.hip", "gbla_api.cpp", "gbla_plan.h"):
+    for f in ("gbla_kernels.hip", "gbla_stream.hip", "gbla_device.h", "gbla_api.cpp", "gbla_plan.h"):
         with open(os.path.join(ROOT, "paper_2606_07317_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -97,6 +97,9 @@ def main():
     ap.add_argument("--sets", type=int, default=0, help="rotated input sets (0: enough for 1 GiB)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only copy 256 MiB device-to-device --steps times (reference for "
+                         "rocprofv3 FETCH_SIZE / WRITE_SIZE scaling)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -110,6 +113,16 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
     dev = torch.device("cuda:0")
+    if args.calibrate_copy:
+        n = 1 << 26  # 64 Mi floats = 256 MiB each way
+        src = torch.ones(n, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        for _ in range(args.steps):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibrate_copy_bytes_each_way": 4 * n, "copies": args.steps}))
+        return
     wname = args.workload or inputs.THROUGHPUT_WORKLOAD
     inp = inputs.make_inputs(wname)
     w = inp.workload
@@ -184,10 +197,10 @@ def main():
                    "forward_effective_GBps": round(fwd_gbps, 1),
                    "forward_hbm_frac": round(fwd_gbps / HBM_PEAK_GBPS, 4),
                    "wall_s": round(wall, 4)},
-        "roofline": {"bound": "hbm", "kernel": "readout_kernel", "achieved": round(ach, 1),
+        "roofline": {"bound": "hbm", "kernel": "readout_stream_kernel", "achieved": round(ach, 1),
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBPS, 4),
                      "avg_launch_ms": readout_ms,
-                     "traffic": traffic_from_profiles("readout_kernel", w.name)},
+                     "traffic": traffic_from_profiles("readout_stream_kernel", w.name)},
     }
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(inp, args.cpu_seconds)

@@ -35,6 +35,23 @@ __device__ __forceinline__ u32x4_t load16(const void* p) {
   return *reinterpret_cast<const u32x4_t*>(p);
 }
 
+// Raw buffer resource over `bytes` bytes from `base` (gfx9 dword-3 format
+// bits).  Loads past the range read 0 and stores past it are dropped, which
+// is how the streaming kernels mask sequence edges without branches.  Byte
+// offsets are 32-bit: callers keep every slice under 2^31 bytes, so a
+// negative offset (a row before the sequence start) is out of range too.
+// The caller passes wave-uniform values; they are moved to scalar registers
+// here so the descriptor never lives in vector registers.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  const uint64_t a = reinterpret_cast<uint64_t>(base);
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)a);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(a >> 32));
+  const int n = __builtin_amdgcn_readfirstlane((int)bytes);
+  void* p = reinterpret_cast<void*>(((uint64_t)hi << 32) | lo);
+  return __builtin_amdgcn_make_buffer_rsrc(p, 0, n, 0x00020000);
+}
+constexpr uint32_t kOutOfRange = 0x80000000u;
+
 // Taps of one tensor (0 = q, 1 = k, 2 = v), head h, channel c, right-aligned
 // to four taps: tap 3 multiplies the current token, taps before 4 - W are 0.
 __device__ __forceinline__ void load_taps4(const float* conv_w, int H, int h, int tensor, int D,
@@ -43,7 +60,8 @@ __device__ __forceinline__ void load_taps4(const float* conv_w, int H, int h, in
 #pragma unroll
   for (int t = 0; t < 4; ++t) {
     const int ti = t - (4 - W);
-    w4[t] = ti >= 0 ? src[ti] : 0.0f;
+    const float x = src[ti < 0 ? 0 : ti];  // unconditional load, then select
+    w4[t] = ti >= 0 ? x : 0.0f;
   }
 }
 
@@ -69,25 +87,35 @@ __device__ __forceinline__ int wave_incl_scan(int x) {
   return x;
 }
 
+// Block-wide reductions for blocks of NT threads (NT / 64 waves); `red`
+// holds NT / 64 entries.
+template <int NT = kThreads>
 __device__ __forceinline__ float block_max(float x, float* red) {
   x = wave_max(x);
   __syncthreads();
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = x;
   __syncthreads();
-  return fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+  float m = red[0];
+#pragma unroll
+  for (int i = 1; i < NT / 64; ++i) m = fmaxf(m, red[i]);
+  return m;
 }
 
 // Inclusive scan over the block; *total receives the block sum.
+template <int NT = kThreads>
 __device__ __forceinline__ int block_incl_scan(int x, int* red, int* total) {
   x = wave_incl_scan(x);
   __syncthreads();
   if ((threadIdx.x & 63) == 63) red[threadIdx.x >> 6] = x;
   __syncthreads();
   const int w = threadIdx.x >> 6;
-  int before = 0;
+  int before = 0, all = 0;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) before += i < w ? red[i] : 0;
-  *total = red[0] + red[1] + red[2] + red[3];
+  for (int i = 0; i < NT / 64; ++i) {
+    before += i < w ? red[i] : 0;
+    all += red[i];
+  }
+  *total = all;
   return x + before;
 }
 
@@ -100,18 +128,19 @@ __device__ __forceinline__ int units_of(int64_t len, int unit) {
 // g-th unit of a head, where sequence s owns max(1, ceil(len_s / unit))
 // consecutive units.  Every thread of the block must call it; returns false
 // (for the whole block) when g is past the last unit.
+template <int NT = kThreads>
 __device__ __forceinline__ bool locate_unit(const int32_t* cu, int nseq, int unit, int g,
                                             int* s_out, int* idx_out) {
-  __shared__ int red[4];
+  __shared__ int red[NT / 64];
   __shared__ int found[2];
   if (threadIdx.x == 0) found[0] = -1;
   int running = 0;
-  for (int base = 0; base < nseq; base += kThreads) {
+  for (int base = 0; base < nseq; base += NT) {
     const int s = base + threadIdx.x;
     int cnt = 0;
     if (s < nseq) cnt = units_of((int64_t)cu[s + 1] - cu[s], unit);
     int total;
-    const int incl = block_incl_scan(cnt, red, &total);
+    const int incl = block_incl_scan<NT>(cnt, red, &total);
     const int excl = incl - cnt;
     if (s < nseq && g >= running + excl && g < running + incl) {
       found[0] = s;
@@ -152,9 +181,10 @@ __device__ __forceinline__ void seq_geometry(const Plan& P, const int32_t* cu, i
 }
 
 // Find (sequence, unit index) of unit g of a head, dense or ragged.
+template <int NT = kThreads>
 __device__ __forceinline__ bool unit_of(const Plan& P, const int32_t* cu, int unit, int per_seq,
                                         int g, int* s, int* idx) {
-  if (P.ragged) return locate_unit(cu, P.nseq, unit, g, s, idx);
+  if (P.ragged) return locate_unit<NT>(cu, P.nseq, unit, g, s, idx);
   *s = g / per_seq;
   *idx = g - *s * per_seq;
   return true;

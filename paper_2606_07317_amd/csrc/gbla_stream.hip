@@ -16,6 +16,14 @@
 // gate weight are applied in registers and the results are already the
 // operands of v_mfma_f32_32x32x16_bf16: A = w phi(kt) (channel c, 8 tokens),
 // B = vt as bf16 hi + bf16 lo (channel e, 8 tokens).
+//
+// readout_stream_kernel: see its own comment below.
+//
+// All global traffic of the hot loops goes through raw buffer descriptors
+// that span one (sequence, head) slice: rows before the sequence start or
+// past its end read as zero, stores past the tile end are dropped.  There
+// are no branches around memory instructions, so the compiler's wait counts
+// stay exact and the prefetched loads remain in flight.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -27,6 +35,15 @@
 namespace gbla {
 namespace {
 
+__device__ __forceinline__ u32x4_t bload16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+}
+
+__device__ __forceinline__ i16x4_t tr_read(const unsigned char* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) i16x4_t*)(p));
+}
+
 template <int D>
 struct SS {
   static constexpr int kStep = 16;                     // tokens per MFMA K block
@@ -37,9 +54,11 @@ struct SS {
   static constexpr int kSlots = 4;                      // ring depth
   static constexpr int kRing = 2 * kSlots * kSlotBytes; // k and v rings of one wave
   static constexpr int kT = D / 32;                     // 32-wide MFMA tiles per side
+  static constexpr int kWaves = 4;                      // waves per workgroup
+  static constexpr int kNT = 64 * kWaves;
   static constexpr int kMaxQ = 512;                     // tokens per wave (chunk <= 2048)
   static constexpr int kWaveBytes = kRing > D * D * 4 ? kRing : D * D * 4;
-  static constexpr int kLds = 4 * kWaveBytes + 4 * kMaxQ * 4;
+  static constexpr int kLds = kWaves * kWaveBytes + kWaves * kMaxQ * 4;
 };
 
 // Byte offset of element e (a multiple of 4) of row r inside a slot, with the
@@ -51,48 +70,64 @@ __device__ __forceinline__ int swz(int r, int e) {
   return r * C::kRowBytes + ((c ^ (r & (C::kChunks - 1))) << 4) + (half << 3);
 }
 
-__device__ __forceinline__ i16x4_t tr_read(const unsigned char* p) {
-  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-      (__attribute__((address_space(3))) i16x4_t*)(p));
-}
-
 template <int D>
-__global__ void __launch_bounds__(kThreads, 2)
+__global__ void __launch_bounds__(SS<D>::kNT, 1)
 state_stream_kernel(Plan P, const uint16_t* __restrict__ kin, const uint16_t* __restrict__ vin,
                     const uint16_t* __restrict__ ain, const float* __restrict__ conv_w,
                     const int32_t* __restrict__ cu, float* __restrict__ partials) {
   using C = SS<D>;
   constexpr int kT = C::kT;
   __shared__ __attribute__((aligned(16))) unsigned char lds[C::kLds];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int h = blockIdx.y, g = blockIdx.x;
   int s, chunk;
-  if (!unit_of(P, cu, P.chunk, P.chunks_per_seq, g, &s, &chunk)) return;
+  if (!unit_of<C::kNT>(P, cu, P.chunk, P.chunks_per_seq, g, &s, &chunk)) return;
+  s = __builtin_amdgcn_readfirstlane(s);
+  chunk = __builtin_amdgcn_readfirstlane(chunk);
   int64_t len, base_row;
   seq_geometry(P, cu, s, h, &len, &base_row);
   const int64_t t0 = (int64_t)chunk * P.chunk;
   const int64_t t1 = min(len, t0 + (int64_t)P.chunk);
   float* rec = partials + ((size_t)h * P.units + g) * P.rec_floats;
 
-  const int Q = P.chunk >> 2;                      // tokens per wave
-  const int64_t w0 = t0 + (int64_t)wave * Q;
-  const int64_t w1 = min(t1, w0 + Q);
-  const int nsteps = w1 > w0 ? (int)((w1 - w0 + C::kStep - 1) / C::kStep) : 0;
+  const int Q = P.chunk / C::kWaves;               // tokens per wave
+  const int w0 = (int)(t0 + (int64_t)wave * Q);    // slice-relative token range
+  const int w1 = (int)min(t1, (int64_t)w0 + Q);
+  const int nsteps = w1 > w0 ? (w1 - w0 + C::kStep - 1) / C::kStep : 0;
   unsigned char* ring = lds + wave * C::kWaveBytes;  // [2 tensors][kSlots][slot]
-  float* wbuf = reinterpret_cast<float*>(lds + 4 * C::kWaveBytes) + wave * C::kMaxQ;
+  float* wbuf = reinterpret_cast<float*>(lds + C::kWaves * C::kWaveBytes) + wave * C::kMaxQ;
+
+  const __amdgpu_buffer_rsrc_t rk = make_rsrc(kin + base_row * D, (uint32_t)(len * C::kRowBytes));
+  const __amdgpu_buffer_rsrc_t rv = make_rsrc(vin + base_row * D, (uint32_t)(len * C::kRowBytes));
+  const __amdgpu_buffer_rsrc_t ra = make_rsrc(ain + base_row, (uint32_t)(len * 2));
+
+  // Loop-invariant global values first (taps, gate logits), so that the
+  // waits for them precede every prefetch.
+  float wk[kT][4], wvt[kT][4];
+#pragma unroll
+  for (int t = 0; t < kT; ++t) {
+    load_taps4(conv_w, P.heads, h, 1, D, P.W, 32 * t + (lane & 31), wk[t]);
+    load_taps4(conv_w, P.heads, h, 2, D, P.W, 32 * t + (lane & 31), wvt[t]);
+  }
+  uint32_t abits[C::kMaxQ / 64];
+#pragma unroll
+  for (int i = 0; i < C::kMaxQ / 64; ++i) {
+    const int tok = w0 + lane + 64 * i;
+    abits[i] = __builtin_amdgcn_raw_buffer_load_b16(ra, (uint32_t)tok * 2u, 0, 0);
+  }
 
   // ---- register-staged loads of one step (rows w0 + 16*step + [0, 16)) ----
   u32x4_t stage[2][2][C::kVec];  // [in-flight buffer][tensor][vector]
-  auto issue = [&](int step, int buf) {
+  auto issue = [&](int step, int buf, int first_row) {
 #pragma unroll
     for (int x = 0; x < C::kVec; ++x) {
       const int u = x * 64 + lane;
       const int row = u / C::kChunks, ch = u % C::kChunks;
-      const int64_t tok = w0 + (int64_t)step * C::kStep + row;
-      const bool ok = tok >= 0 && tok < len;
-      const size_t off = (size_t)(base_row + tok) * D + ch * 8;
-      stage[buf][0][x] = ok ? load16(kin + off) : u32x4_t{0u, 0u, 0u, 0u};
-      stage[buf][1][x] = ok ? load16(vin + off) : u32x4_t{0u, 0u, 0u, 0u};
+      const int tok = w0 + step * C::kStep + row;
+      const uint32_t off = row >= first_row ? (uint32_t)(tok * D + ch * 8) * 2u : kOutOfRange;
+      stage[buf][0][x] = bload16(rk, off);
+      stage[buf][1][x] = bload16(rv, off);
     }
   };
   auto commit = [&](int step, int buf) {
@@ -109,18 +144,18 @@ state_stream_kernel(Plan P, const uint16_t* __restrict__ kin, const uint16_t* __
     }
   };
 
-  if (nsteps > 0) {
-    issue(-1, 1);
-    issue(0, 0);
-  }
+  // Only rows 12..15 of the step before the wave's first token are needed
+  // (the conv window); the others are masked off.
+  issue(-1, 1, nsteps > 0 ? C::kStep - 4 : C::kStep);
+  issue(0, 0, nsteps > 0 ? 0 : C::kStep);
 
   // ---- gate weights of the wave's tokens: m_w, w_j = exp(a_j - m_w), l_w ----
   float av[C::kMaxQ / 64];
   float mloc = -INFINITY;
 #pragma unroll
   for (int i = 0; i < C::kMaxQ / 64; ++i) {
-    const int64_t tok = w0 + lane + 64 * i;
-    av[i] = (64 * i < Q && tok < w1) ? __uint_as_float((uint32_t)ain[base_row + tok] << 16) : -INFINITY;
+    const int tok = w0 + lane + 64 * i;
+    av[i] = (64 * i < Q && tok < w1) ? __uint_as_float(abits[i] << 16) : -INFINITY;
     mloc = fmaxf(mloc, av[i]);
   }
   const float mw = wave_max(mloc);
@@ -135,13 +170,6 @@ state_stream_kernel(Plan P, const uint16_t* __restrict__ kin, const uint16_t* __
   }
   const float lw = wave_sum(lsum);
 
-  float wk[kT][4], wvt[kT][4];
-#pragma unroll
-  for (int t = 0; t < kT; ++t) {
-    load_taps4(conv_w, P.heads, h, 1, D, P.W, 32 * t + (lane & 31), wk[t]);
-    load_taps4(conv_w, P.heads, h, 2, D, P.W, 32 * t + (lane & 31), wvt[t]);
-  }
-
   f32x16_t acc[kT][kT];
 #pragma unroll
   for (int a = 0; a < kT; ++a)
@@ -153,12 +181,10 @@ state_stream_kernel(Plan P, const uint16_t* __restrict__ kin, const uint16_t* __
 #pragma unroll
   for (int t = 0; t < kT; ++t) zacc[t] = 0.0f;
 
-  if (nsteps > 0) {
-    commit(-1, 1);
-    if (nsteps > 1) issue(1, 1);
-    commit(0, 0);
-    if (nsteps > 2) issue(2, 0);
-  }
+  commit(-1, 1);
+  issue(1, 1, nsteps > 1 ? 0 : C::kStep);
+  commit(0, 0);
+  issue(2, 0, nsteps > 2 ? 0 : C::kStep);
 
   // Lane roles for the transposed reads and the MFMA operands.
   const int half = lane >> 5;             // token half of the 16-token step
@@ -230,11 +256,11 @@ state_stream_kernel(Plan P, const uint16_t* __restrict__ kin, const uint16_t* __
             __builtin_bit_cast(bf16x8_t, A[a]), __builtin_bit_cast(bf16x8_t, Bl[b]), acc[a][b], 0, 0, 0);
       }
     // Stage step i+1 into the ring (its slot held step i-3) and refill the
-    // freed registers with step i+3.
-    if (i + 1 < nsteps) {
-      commit(i + 1, kNext);
-      if (i + 3 < nsteps) issue(i + 3, kNext);
-    }
+    // freed registers with step i+3.  Both run unconditionally so the wait
+    // counts are the same on every path; steps past the end are loaded with
+    // every row out of range (no memory traffic, zeros).
+    commit(i + 1, kNext);
+    issue(i + 3, kNext, i + 3 < nsteps ? 0 : C::kStep);
   };
   int i = 0;
   for (; i + 1 < nsteps; i += 2) {
@@ -253,10 +279,10 @@ state_stream_kernel(Plan P, const uint16_t* __restrict__ kin, const uint16_t* __
 #pragma unroll
     for (int b = 0; b < kT; ++b)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int c = 32 * a + 8 * (i / 4) + 4 * half + (i % 4);
+      for (int q = 0; q < 16; ++q) {
+        const int c = 32 * a + 8 * (q / 4) + 4 * half + (q % 4);
         const int e = 32 * b + (lane & 31);
-        Sw[c * D + e] = acc[a][b][i];
+        Sw[c * D + e] = acc[a][b][q];
       }
   float* zw = wbuf;  // reuse: z_w[D], m_w, l_w
   if (lane < 32) {
@@ -268,35 +294,35 @@ state_stream_kernel(Plan P, const uint16_t* __restrict__ kin, const uint16_t* __
     zw[D + 1] = lw;
   }
   __syncthreads();
-  float mws[4], f[4];
+  const float* wb0 = reinterpret_cast<const float*>(lds + C::kWaves * C::kWaveBytes);
+  float mws[C::kWaves], f[C::kWaves];
   float M = -INFINITY;
 #pragma unroll
-  for (int w = 0; w < 4; ++w) {
-    mws[w] = reinterpret_cast<const float*>(lds + 4 * C::kWaveBytes)[w * C::kMaxQ + D];
+  for (int w = 0; w < C::kWaves; ++w) {
+    mws[w] = wb0[w * C::kMaxQ + D];
     M = fmaxf(M, mws[w]);
   }
 #pragma unroll
-  for (int w = 0; w < 4; ++w) f[w] = mws[w] == -INFINITY ? 0.0f : __expf(mws[w] - M);
+  for (int w = 0; w < C::kWaves; ++w) f[w] = mws[w] == -INFINITY ? 0.0f : __expf(mws[w] - M);
 #pragma unroll
-  for (int k = 0; k < D * D / kThreads; ++k) {
-    const int x = k * kThreads + tid;
+  for (int k = 0; k < D * D / C::kNT; ++k) {
+    const int x = k * C::kNT + tid;
     float v = 0.0f;
 #pragma unroll
-    for (int w = 0; w < 4; ++w)
+    for (int w = 0; w < C::kWaves; ++w)
       v = fmaf(f[w], reinterpret_cast<const float*>(lds + w * C::kWaveBytes)[x], v);
     rec[x] = v;
   }
-  const float* wb0 = reinterpret_cast<const float*>(lds + 4 * C::kWaveBytes);
   if (tid < D) {
     float v = 0.0f;
 #pragma unroll
-    for (int w = 0; w < 4; ++w) v = fmaf(f[w], wb0[w * C::kMaxQ + tid], v);
+    for (int w = 0; w < C::kWaves; ++w) v = fmaf(f[w], wb0[w * C::kMaxQ + tid], v);
     rec[D * D + tid] = v;
   }
   if (tid == 0) {
     float l = 0.0f;
 #pragma unroll
-    for (int w = 0; w < 4; ++w) l = fmaf(f[w], wb0[w * C::kMaxQ + D + 1], l);
+    for (int w = 0; w < C::kWaves; ++w) l = fmaf(f[w], wb0[w * C::kMaxQ + D + 1], l);
     rec[D * D + D] = M;
     rec[D * D + D + 1] = l;
   }
@@ -308,9 +334,9 @@ state_stream_kernel(Plan P, const uint16_t* __restrict__ kin, const uint16_t* __
 //   o_i = phi(qt_i)^T S / phi(qt_i)^T z,
 //   y_i = o_i / sqrt(mean_e o_i^2 + eps) * gamma * SiLU(r_i)
 // q rows are staged through a per-wave LDS ring (register-staged loads one
-// group ahead, 16-byte chunks XOR-swizzled by row; r one group ahead); each lane reads the
-// four rows of its token's conv window, so lane (n, gq) gets phi(qt) of token
-// n for channels 32*kb + 8*gq + [0, 8): the B operand of
+// group ahead, 16-byte chunks XOR-swizzled by row; r one group ahead); each
+// lane reads the four rows of its token's conv window, so lane (n, gq) gets
+// phi(qt) of token n for channels 32*kb + 8*gq + [0, 8): the B operand of
 // v_mfma_f32_16x16x32_bf16.  The A operands [S^T; z^T] stay in registers
 // for the whole tile.  The gated-RMSNorm epilogue reduces each token's
 // squares over the four lanes that hold its 64 (or 32) channels.
@@ -337,10 +363,13 @@ readout_stream_kernel(Plan P, const uint16_t* __restrict__ qin, const uint16_t* 
   __shared__ __attribute__((aligned(16))) unsigned char lds[C::kLds];
   __shared__ __attribute__((aligned(16))) float taps_q[D][4];  // right-aligned, tap 3 = current
   __shared__ __attribute__((aligned(16))) float gam[D];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int h = blockIdx.y, g = blockIdx.x;
   int s, tile;
   if (!unit_of(P, cu, P.rtile, P.rtiles_per_seq, g, &s, &tile)) return;
+  s = __builtin_amdgcn_readfirstlane(s);
+  tile = __builtin_amdgcn_readfirstlane(tile);
   if (tid < D) {
     load_taps4(conv_w, P.heads, h, 0, D, P.W, tid, taps_q[tid]);
     gam[tid] = gamma[(size_t)h * D + tid];
@@ -351,37 +380,47 @@ readout_stream_kernel(Plan P, const uint16_t* __restrict__ qin, const uint16_t* 
   const int64_t tt0 = (int64_t)tile * P.rtile;
   const int64_t tt1 = min(len, tt0 + (int64_t)P.rtile);
   const int per_wave = P.rtile >> 2;
-  const int64_t r0 = tt0 + (int64_t)wave * per_wave;
-  const int64_t r1 = min(tt1, r0 + per_wave);
+  const int r0 = (int)(tt0 + (int64_t)wave * per_wave);  // slice-relative
+  const int r1 = (int)min(tt1, (int64_t)r0 + per_wave);
   if (r1 <= r0) return;  // no block-wide synchronisation follows
-  const int ngroups = (int)((r1 - r0 + C::kGroup - 1) / C::kGroup);
+  const int ngroups = (r1 - r0 + C::kGroup - 1) / C::kGroup;
   unsigned char* ring = lds + wave * C::kSlots * C::kSlotBytes;
 
   const int n = lane & 15, gq = lane >> 4;
   const size_t sh = (size_t)s * P.heads + h;
+  const __amdgpu_buffer_rsrc_t rq = make_rsrc(qin + base_row * D, (uint32_t)(len * C::kRowBytes));
+  const __amdgpu_buffer_rsrc_t rr = make_rsrc(rin + base_row * D, (uint32_t)(len * C::kRowBytes));
+  // stores of tokens at or past r1 fall outside this range and are dropped
+  const __amdgpu_buffer_rsrc_t ro = make_rsrc(out + base_row * D, (uint32_t)r1 * (uint32_t)(4 * D));
+
+  // Readout operands [S^T; z^T]: loaded before any prefetch so that their
+  // wait precedes the pipeline.
+  const unsigned char* fr = frags + sh * P.frag_bytes;
+  u32x4_t A[NMB][NKB];
+#pragma unroll
+  for (int mb = 0; mb < NMB; ++mb)
+#pragma unroll
+    for (int kb = 0; kb < NKB; ++kb) A[mb][kb] = load16(fr + (((size_t)mb * NKB + kb) * 64 + lane) * 16);
 
   // ---- staged loads: q rows of a group, r chunks of the lane's two tokens ----
   u32x4_t qst[C::kVec];
   u32x4_t rst[2][NKB];
-  auto issue_q = [&](int grp) {
+  auto issue_q = [&](int grp, int first_row) {
 #pragma unroll
     for (int x = 0; x < C::kVec; ++x) {
       const int u = x * 64 + lane;
       const int row = u / C::kChunks, ch = u % C::kChunks;
-      const int64_t tok = r0 + (int64_t)grp * C::kGroup + row;
-      const bool ok = tok >= 0 && tok < len;
-      qst[x] = ok ? load16(qin + (size_t)(base_row + tok) * D + ch * 8) : u32x4_t{0u, 0u, 0u, 0u};
+      const int tok = r0 + grp * C::kGroup + row;
+      qst[x] = bload16(rq, row >= first_row ? (uint32_t)(tok * D + ch * 8) * 2u : kOutOfRange);
     }
   };
-  auto issue_r = [&](int grp) {
+  auto issue_r = [&](int grp, bool live) {
 #pragma unroll
     for (int jb = 0; jb < 2; ++jb) {
-      const int64_t tok = r0 + (int64_t)grp * C::kGroup + 16 * jb + n;
-      const bool ok = tok < r1;
+      const int tok = r0 + grp * C::kGroup + 16 * jb + n;
 #pragma unroll
       for (int qq = 0; qq < NKB; ++qq)
-        rst[jb][qq] = ok ? load16(rin + (size_t)(base_row + tok) * D + 32 * qq + 8 * gq)
-                              : u32x4_t{0u, 0u, 0u, 0u};
+        rst[jb][qq] = bload16(rr, live ? (uint32_t)(tok * D + 32 * qq + 8 * gq) * 2u : kOutOfRange);
     }
   };
   auto commit_q = [&](int grp) {
@@ -395,21 +434,13 @@ readout_stream_kernel(Plan P, const uint16_t* __restrict__ qin, const uint16_t* 
     }
   };
 
-  issue_q(-1);
-  issue_r(0);
-
-  // Readout operands [S^T; z^T], conv taps and gamma of the lane's channels.
-  const unsigned char* fr = frags + sh * P.frag_bytes;
-  u32x4_t A[NMB][NKB];
-#pragma unroll
-  for (int mb = 0; mb < NMB; ++mb)
-#pragma unroll
-    for (int kb = 0; kb < NKB; ++kb) A[mb][kb] = load16(fr + (((size_t)mb * NKB + kb) * 64 + lane) * 16);
-
+  // Rows 29..31 of the group before the wave's first token (the conv window).
+  issue_q(-1, C::kGroup - 3);
   commit_q(-1);
-  issue_q(0);
+  issue_q(0, 0);
+  issue_r(0, true);
   commit_q(0);
-  if (ngroups > 1) issue_q(1);
+  issue_q(1, ngroups > 1 ? 0 : C::kGroup);
 
   for (int grp = 0; grp < ngroups; ++grp) {
     const unsigned char* cur = ring + (grp % C::kSlots) * C::kSlotBytes;
@@ -429,10 +460,10 @@ readout_stream_kernel(Plan P, const uint16_t* __restrict__ qin, const uint16_t* 
         for (int t = 0; t < 4; ++t) {
           const int rw = row - 3 + t;
           const unsigned char* base = rw < 0 ? prv : cur;
-          const int rr = rw < 0 ? rw + C::kGroup : rw;
+          const int rrow = rw < 0 ? rw + C::kGroup : rw;
           const int ch = 4 * kb + gq;
           const u32x4_t u = *reinterpret_cast<const u32x4_t*>(
-              base + rr * C::kRowBytes + ((ch ^ (rr & (C::kChunks - 1))) << 4));
+              base + rrow * C::kRowBytes + ((ch ^ (rrow & (C::kChunks - 1))) << 4));
 #pragma unroll
           for (int w = 0; w < 4; ++w) {
             x[t][2 * w] = bf16_lo(u[w]);
@@ -476,45 +507,44 @@ readout_stream_kernel(Plan P, const uint16_t* __restrict__ qin, const uint16_t* 
       ss += __shfl_xor(ss, 16);
       ss += __shfl_xor(ss, 32);
       const float scale = __builtin_amdgcn_rsqf(ss * (1.0f / D) + P.eps);
-      const int64_t tok = r0 + (int64_t)grp * C::kGroup + row;
-      if (tok < r1) {
-        float* dst = out + (size_t)(base_row + tok) * D + 8 * gq;
+      const int tok = r0 + grp * C::kGroup + row;
 #pragma unroll
-        for (int qq = 0; qq < NKB; ++qq) {
-          const u32x4_t rw = rst[jb][qq];
-          const f32x4_t g0 = *reinterpret_cast<const f32x4_t*>(&gam[32 * qq + 8 * gq]);
-          const f32x4_t g1 = *reinterpret_cast<const f32x4_t*>(&gam[32 * qq + 8 * gq + 4]);
-          f32x4_t y0, y1;
+      for (int qq = 0; qq < NKB; ++qq) {
+        const u32x4_t rw = rst[jb][qq];
+        const f32x4_t g0 = *reinterpret_cast<const f32x4_t*>(&gam[32 * qq + 8 * gq]);
+        const f32x4_t g1 = *reinterpret_cast<const f32x4_t*>(&gam[32 * qq + 8 * gq + 4]);
+        f32x4_t y0, y1;
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const float ra = i & 1 ? bf16_hi(rw[i >> 1]) : bf16_lo(rw[i >> 1]);
-            const float rb = i & 1 ? bf16_hi(rw[2 + (i >> 1)]) : bf16_lo(rw[2 + (i >> 1)]);
-            const float sa = ra * __builtin_amdgcn_rcpf(1.0f + __expf(-ra));
-            const float sb = rb * __builtin_amdgcn_rcpf(1.0f + __expf(-rb));
-            y0[i] = acc[2 * qq][i] * scale * g0[i] * sa;
-            y1[i] = acc[2 * qq + 1][i] * scale * g1[i] * sb;
-          }
-          f32x4_t* d4 = reinterpret_cast<f32x4_t*>(dst + 32 * qq);
-          d4[0] = y0;
-          d4[1] = y1;
+        for (int i = 0; i < 4; ++i) {
+          const float ra = i & 1 ? bf16_hi(rw[i >> 1]) : bf16_lo(rw[i >> 1]);
+          const float rb = i & 1 ? bf16_hi(rw[2 + (i >> 1)]) : bf16_lo(rw[2 + (i >> 1)]);
+          const float sa = ra * __builtin_amdgcn_rcpf(1.0f + __expf(-ra));
+          const float sb = rb * __builtin_amdgcn_rcpf(1.0f + __expf(-rb));
+          y0[i] = acc[2 * qq][i] * scale * g0[i] * sa;
+          y1[i] = acc[2 * qq + 1][i] * scale * g1[i] * sb;
         }
+        const uint32_t off = (uint32_t)(tok * D + 32 * qq + 8 * gq) * 4u;
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, y0), ro, off, 0, 0);
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, y1), ro, off + 16, 0, 0);
       }
     }
     // Stage group grp+1 into the ring (its slot held group grp-2), then
-    // refill the registers: q rows of group grp+2, r of group grp+1.
-    if (grp + 1 < ngroups) {
-      commit_q(grp + 1);
-      if (grp + 2 < ngroups) issue_q(grp + 2);
-      issue_r(grp + 1);
-    }
+    // refill the registers: r of group grp+1 first, q rows of group grp+2
+    // (fully out of range past the end, so the wait counts never change).
+    commit_q(grp + 1);
+    issue_r(grp + 1, grp + 1 < ngroups);
+    issue_q(grp + 2, grp + 2 < ngroups ? 0 : C::kGroup);
   }
 }
 
 }  // namespace
 
 bool stream_supported(const Plan& p) {
-  return p.dtype == GBLA_BF16 && (p.d == 32 || p.d == 64) && p.chunk <= 4 * SS<64>::kMaxQ &&
-         p.chunk % 64 == 0 && p.rtile % 128 == 0;
+  // Every (sequence, head) slice must stay below 2^31 bytes for the 32-bit
+  // buffer offsets; the fp32 output rows are the widest.
+  return p.dtype == GBLA_BF16 && (p.d == 32 || p.d == 64) &&
+         p.chunk <= SS<64>::kWaves * SS<64>::kMaxQ && p.chunk % (16 * SS<64>::kWaves) == 0 &&
+         p.rtile % 128 == 0 && (int64_t)p.rows * p.d * 4 < (int64_t(1) << 31);
 }
 
 gbla_status launch_state_stream(const Plan& p, const void* k, const void* v, const void* a,
@@ -522,17 +552,13 @@ gbla_status launch_state_stream(const Plan& p, const void* k, const void* v, con
                                 hipStream_t st) {
   const dim3 grid(p.units, p.heads);
   if (p.d == 64)
-    hipLaunchKernelGGL((state_stream_kernel<64>), grid, dim3(kThreads), 0, st, p,
+    hipLaunchKernelGGL((state_stream_kernel<64>), grid, dim3(SS<64>::kNT), 0, st, p,
                        (const uint16_t*)k, (const uint16_t*)v, (const uint16_t*)a, conv_w, cu, partials);
   else
-    hipLaunchKernelGGL((state_stream_kernel<32>), grid, dim3(kThreads), 0, st, p,
+    hipLaunchKernelGGL((state_stream_kernel<32>), grid, dim3(SS<32>::kNT), 0, st, p,
                        (const uint16_t*)k, (const uint16_t*)v, (const uint16_t*)a, conv_w, cu, partials);
   return hipGetLastError() == hipSuccess ? GBLA_OK : GBLA_ERR_HIP;
 }
-
-}  // namespace gbla
-
-namespace gbla {
 
 gbla_status launch_readout_stream(const Plan& p, const void* q, const void* r, const float* conv_w,
                                   const float* gamma, const int32_t* cu, const unsigned char* frags,
