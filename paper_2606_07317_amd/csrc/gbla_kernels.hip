@@ -426,13 +426,18 @@ __device__ __forceinline__ void frag_put(void* frag_sh, int mb, int kb, int lane
 // grid = (N * H, element slices of 64).  Thread (x, pg) of a block sums the
 // element x of partials pg, pg + 4, ... (in that order) scaled by
 // exp(m_p - M); the four sums are added in the order pg = 0..3, then divided
-// by Z = sum_p exp(m_p - M) l_p.  The split of the partials is a function of
+// by Z = sum_p exp(m_p - M) l_p.  The partials are taken in rounds of 32:
+// every load of a round (m_p, l_p and element x of the thread's eight
+// partials) is issued at once, and a later round with a larger maximum
+// rescales what came before.  The split of the partials is a function of
 // the shape only, so the result is the same on every call.
 template <typename T, int D>
 __global__ void __launch_bounds__(kThreads)
 combine_kernel(Plan P, const int32_t* __restrict__ cu, const float* __restrict__ partials,
                float* __restrict__ S_out, float* __restrict__ z_out, unsigned char* __restrict__ frags) {
   constexpr int kElems = D * D + D;
+  constexpr int kPer = 8;               // partials per thread per round
+  constexpr int kRound = 4 * kPer;      // partials per round
   __shared__ float red[4];
   __shared__ float part[4][64];
   const int tid = threadIdx.x;
@@ -447,33 +452,52 @@ combine_kernel(Plan P, const int32_t* __restrict__ cu, const float* __restrict__
     count = P.chunks_per_seq;
   }
   const float* recs = partials + ((size_t)h * P.units + first) * P.rec_floats;
-  float mloc = -INFINITY;
-  for (int p = tid; p < count; p += kThreads) mloc = fmaxf(mloc, recs[(size_t)p * P.rec_floats + kElems]);
-  const float M = block_max(mloc, red);
-  float zl = 0.0f;
-  if (M != -INFINITY)
-    for (int p = tid; p < count; p += kThreads) {
-      const float* r = recs + (size_t)p * P.rec_floats + kElems;
-      zl += gexp<T>(r[0] - M) * r[1];
+  const int xl = tid & 63, pg = tid >> 6;
+  const int x = blockIdx.y * 64 + xl;
+  const int xc = x < kElems ? x : 0;    // element read (a valid address for every lane)
+  const float xmask = x < kElems ? 1.0f : 0.0f;
+
+  float M = -INFINITY, zl = 0.0f, v = 0.0f;
+  for (int base = 0; base < count; base += kRound) {
+    float mv[kPer], lv[kPer], ev[kPer], pm[kPer];
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      const int p = base + pg + 4 * j;
+      const float* r = recs + (size_t)(p < count ? p : 0) * P.rec_floats;
+      mv[j] = r[kElems];
+      lv[j] = r[kElems + 1];
+      ev[j] = r[xc];
+      pm[j] = p < count ? 0.0f : -INFINITY;  // added, not selected: the loads stay unconditional
     }
-  zl = wave_sum(zl);
+    float ml = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      mv[j] += pm[j];
+      ml = fmaxf(ml, mv[j]);
+    }
+    const float Mr = block_max(ml, red);
+    const float Mn = fmaxf(M, Mr);
+    if (Mn != -INFINITY) {
+      const float f = M == -INFINITY ? 0.0f : gexp<T>(M - Mn);
+      zl *= f;
+      v *= f;
+#pragma unroll
+      for (int j = 0; j < kPer; ++j) {
+        const float w = mv[j] == -INFINITY ? 0.0f : gexp<T>(mv[j] - Mn);
+        zl = fmaf(w, lv[j], zl);
+        v = fmaf(w, ev[j], v);
+      }
+    }
+    M = Mn;
+  }
+  // Z over the four partial groups: every wave holds the same pg-group sum
+  // in each of its lanes, so lane 0 of each wave contributes once.
   __syncthreads();
   if ((tid & 63) == 0) red[tid >> 6] = zl;
   __syncthreads();
   const float Z = (red[0] + red[1]) + (red[2] + red[3]);
   const float invZ = Z > 0.0f ? 1.0f / Z : 0.0f;
-
-  const int xl = tid & 63, pg = tid >> 6;
-  const int x = blockIdx.y * 64 + xl;
-  float v = 0.0f;
-  if (x < kElems && invZ > 0.0f) {
-#pragma unroll 4
-    for (int p = pg; p < count; p += 4) {
-      const float* r = recs + (size_t)p * P.rec_floats;
-      v = fmaf(gexp<T>(r[kElems] - M), r[x], v);
-    }
-  }
-  part[pg][xl] = v;
+  part[pg][xl] = v * xmask;
   __syncthreads();
   if (tid >= 64 || x >= kElems) return;
   const float val = (((part[0][xl] + part[1][xl]) + part[2][xl]) + part[3][xl]) * invZ;

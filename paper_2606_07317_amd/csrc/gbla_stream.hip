@@ -6,16 +6,25 @@
 // form K^T V and K^T 1 with K = g (.) phi(K)):
 //     S_p = sum_j w_j phi(kt_j) vt_j^T,  z_p = sum_j w_j phi(kt_j),
 //     w_j = exp(a_j - m_p),  m_p = max_j a_j,  l_p = sum_j w_j.
-// Each of the four waves owns a quarter of the chunk and never waits for the
-// others until the final merge.  A wave streams its tokens 16 at a time:
-// raw bf16 k and v rows are loaded two steps ahead into registers, written
-// row-major into a per-wave LDS ring (16-byte chunks XOR-swizzled by row),
-// and read back with ds_read_b64_tr_b16, which hands each lane four
-// consecutive tokens of one channel.  Twelve tokens (three reads) give the
-// lane the causal conv window of its eight tokens, so the conv, phi and the
-// gate weight are applied in registers and the results are already the
-// operands of v_mfma_f32_32x32x16_bf16: A = w phi(kt) (channel c, 8 tokens),
-// B = vt as bf16 hi + bf16 lo (channel e, 8 tokens).
+// The chunk is split into token parts; the two waves of a part share its
+// tokens and split the key channels (one 32-channel MFMA tile each), so two
+// waves run on every SIMD and each one's vector work overlaps the other's
+// MFMAs.  A wave streams its tokens 16 at a time: raw bf16 key (its 32
+// channels) and value rows are loaded two steps ahead into registers,
+// written row-major into the wave's LDS rings (16-byte chunks XOR-swizzled
+// by row), and read back with ds_read_b64_tr_b16, which hands each lane four
+// consecutive tokens of one channel.  Twelve key tokens (three reads) give
+// the lane the causal conv window of its eight tokens, so the key conv, phi
+// and the gate weight are applied in registers and the results are already
+// the A operand of v_mfma_f32_32x32x16_bf16 (channel c, 8 tokens).
+// The value conv is linear and acts channel by channel, so it is moved past
+// the token sum: with taps u_tau (tap 3 on the current token),
+//     S_p[c][e] = sum_tau u_tau[e] M_tau[c][e],
+//     M_tau     = sum_j w_j phi(kt_j) v_{j-3+tau}^T,
+// and each M_tau is one MFMA accumulator fed with raw bf16 v rows read at a
+// shift of tau - 3 tokens.  The value path costs no vector ALU work in the
+// loop and v enters the products exactly; the taps are applied once, in fp32,
+// when the accumulators are merged.
 //
 // readout_stream_kernel: see its own comment below.
 //
@@ -46,28 +55,35 @@ __device__ __forceinline__ i16x4_t tr_read(const unsigned char* p) {
 
 template <int D>
 struct SS {
-  static constexpr int kStep = 16;                     // tokens per MFMA K block
-  static constexpr int kRowBytes = 2 * D;               // one bf16 row
-  static constexpr int kChunks = kRowBytes / 16;        // 16-byte chunks per row
-  static constexpr int kSlotBytes = kStep * kRowBytes;  // one step of one tensor
-  static constexpr int kVec = kSlotBytes / (64 * 16);   // 16-byte vectors per lane per step
-  static constexpr int kSlots = 4;                      // ring depth
-  static constexpr int kRing = 2 * kSlots * kSlotBytes; // k and v rings of one wave
-  static constexpr int kT = D / 32;                     // 32-wide MFMA tiles per side
-  static constexpr int kWaves = 4;                      // waves per workgroup
+  static constexpr int kStep = 16;                       // tokens per MFMA K block
+  static constexpr int kKH = D / 32;                      // waves sharing a token part
+  static constexpr int kWaves = 8;                        // two per SIMD
   static constexpr int kNT = 64 * kWaves;
-  static constexpr int kMaxQ = 512;                     // tokens per wave (chunk <= 2048)
-  static constexpr int kWaveBytes = kRing > D * D * 4 ? kRing : D * D * 4;
-  static constexpr int kLds = kWaves * kWaveBytes + kWaves * kMaxQ * 4;
+  static constexpr int kParts = kWaves / kKH;             // token parts of a chunk
+  static constexpr int kTB = D / 32;                      // 32-wide value tiles
+  static constexpr int kStepBytes = kStep * 2 * D;        // one step of rows in memory
+  static constexpr int kKRow = 64;                        // a wave's 32 key channels of a row
+  static constexpr int kVRow = 2 * D;                     // a value row
+  static constexpr int kKChunks = kKRow / 16, kVChunks = kVRow / 16;
+  static constexpr int kKSlot = kStep * kKRow, kVSlot = kStep * kVRow;
+  static constexpr int kKVec = kKSlot / 1024, kVVec = kVSlot / 1024;  // 16-byte vectors per lane
+  static constexpr int kSlots = 4;                        // ring depth
+  static constexpr int kKRing = kSlots * kKSlot;
+  static constexpr int kRing = kKRing + kSlots * kVSlot;  // one wave's rings
+  static constexpr int kMaxChunk = 2048;
+  static constexpr int kMaxQ = kMaxChunk / kParts;        // tokens per part
+  static constexpr int kPartFloats = D * D + D + 2;       // S, z, m, l of a part
+  static constexpr int kMerge = kParts * kPartFloats * 4;
+  static constexpr int kRings = kWaves * kRing > kMerge ? kWaves * kRing : kMerge;
+  static constexpr int kLds = kRings + kWaves * kMaxQ * 4;
 };
 
-// Byte offset of element e (a multiple of 4) of row r inside a slot, with the
-// 16-byte chunks of each row XOR-swizzled by the row index.
-template <int D>
+// Byte offset of element e (a multiple of 4) of row r of a slot whose rows
+// hold `Chunks` 16-byte chunks, XOR-swizzled by the row index.
+template <int Chunks>
 __device__ __forceinline__ int swz(int r, int e) {
-  using C = SS<D>;
   const int c = e >> 3, half = (e >> 2) & 1;
-  return r * C::kRowBytes + ((c ^ (r & (C::kChunks - 1))) << 4) + (half << 3);
+  return r * Chunks * 16 + ((c ^ (r & (Chunks - 1))) << 4) + (half << 3);
 }
 
 template <int D>
@@ -76,10 +92,11 @@ state_stream_kernel(Plan P, const uint16_t* __restrict__ kin, const uint16_t* __
                     const uint16_t* __restrict__ ain, const float* __restrict__ conv_w,
                     const int32_t* __restrict__ cu, float* __restrict__ partials) {
   using C = SS<D>;
-  constexpr int kT = C::kT;
+  constexpr int kTB = C::kTB;
   __shared__ __attribute__((aligned(16))) unsigned char lds[C::kLds];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int part = wave / C::kKH, kh = wave % C::kKH;
   const int h = blockIdx.y, g = blockIdx.x;
   int s, chunk;
   if (!unit_of<C::kNT>(P, cu, P.chunk, P.chunks_per_seq, g, &s, &chunk)) return;
@@ -91,238 +108,307 @@ state_stream_kernel(Plan P, const uint16_t* __restrict__ kin, const uint16_t* __
   const int64_t t1 = min(len, t0 + (int64_t)P.chunk);
   float* rec = partials + ((size_t)h * P.units + g) * P.rec_floats;
 
-  const int Q = P.chunk / C::kWaves;               // tokens per wave
-  const int w0 = (int)(t0 + (int64_t)wave * Q);    // slice-relative token range
+  const int Q = P.chunk / C::kParts;               // tokens per part
+  const int w0 = (int)(t0 + (int64_t)part * Q);    // slice-relative token range
   const int w1 = (int)min(t1, (int64_t)w0 + Q);
   const int nsteps = w1 > w0 ? (w1 - w0 + C::kStep - 1) / C::kStep : 0;
-  unsigned char* ring = lds + wave * C::kWaveBytes;  // [2 tensors][kSlots][slot]
-  float* wbuf = reinterpret_cast<float*>(lds + C::kWaves * C::kWaveBytes) + wave * C::kMaxQ;
+  // The loop turns the ring once per iteration (kSlots steps), so that every
+  // LDS address is a per-lane base plus an immediate.  Steps past nsteps see
+  // only out-of-range rows and zero gate weights and add nothing.
+  const int nturns = (nsteps + C::kSlots - 1) / C::kSlots;
+  unsigned char* ring = lds + wave * C::kRing;  // [key slots][value slots]
+  float* wbuf = reinterpret_cast<float*>(lds + C::kRings) + wave * C::kMaxQ;
 
-  const __amdgpu_buffer_rsrc_t rk = make_rsrc(kin + base_row * D, (uint32_t)(len * C::kRowBytes));
-  const __amdgpu_buffer_rsrc_t rv = make_rsrc(vin + base_row * D, (uint32_t)(len * C::kRowBytes));
+  const __amdgpu_buffer_rsrc_t rk = make_rsrc(kin + base_row * D, (uint32_t)(len * 2 * D));
+  const __amdgpu_buffer_rsrc_t rv = make_rsrc(vin + base_row * D, (uint32_t)(len * 2 * D));
   const __amdgpu_buffer_rsrc_t ra = make_rsrc(ain + base_row, (uint32_t)(len * 2));
 
   // Loop-invariant global values first (taps, gate logits), so that the
-  // waits for them precede every prefetch.
-  float wk[kT][4], wvt[kT][4];
+  // waits for them precede every prefetch.  The key taps carry a factor
+  // log2(e): the loop then forms kt * log2(e) and phi needs only exp2.  The
+  // value taps are needed only by the final merge.
+  constexpr float kLog2e = 1.4426950408889634f, kLn2 = 0.6931471805599453f;
+  const int kch = 32 * kh + (lane & 31);  // the lane's key channel
+  float wk[4], wv[kTB][4];
+  load_taps4(conv_w, P.heads, h, 1, D, P.W, kch, wk);
 #pragma unroll
-  for (int t = 0; t < kT; ++t) {
-    load_taps4(conv_w, P.heads, h, 1, D, P.W, 32 * t + (lane & 31), wk[t]);
-    load_taps4(conv_w, P.heads, h, 2, D, P.W, 32 * t + (lane & 31), wvt[t]);
-  }
+  for (int b = 0; b < kTB; ++b) load_taps4(conv_w, P.heads, h, 2, D, P.W, 32 * b + (lane & 31), wv[b]);
+  // Gate logits of the part's tokens; tokens outside it read as zero and get
+  // -inf added below (an add, not a select on the loaded value, so that the
+  // loads stay ahead of the prefetches instead of being sunk into branches).
   uint32_t abits[C::kMaxQ / 64];
+  float amask[C::kMaxQ / 64];
 #pragma unroll
   for (int i = 0; i < C::kMaxQ / 64; ++i) {
     const int tok = w0 + lane + 64 * i;
-    abits[i] = __builtin_amdgcn_raw_buffer_load_b16(ra, (uint32_t)tok * 2u, 0, 0);
+    const bool valid = 64 * i < Q && tok < w1;
+    abits[i] = __builtin_amdgcn_raw_buffer_load_b16(ra, valid ? (uint32_t)tok * 2u : kOutOfRange, 0, 0);
+    amask[i] = valid ? 0.0f : -INFINITY;
   }
 
-  // ---- register-staged loads of one step (rows w0 + 16*step + [0, 16)) ----
-  u32x4_t stage[2][2][C::kVec];  // [in-flight buffer][tensor][vector]
-  auto issue = [&](int step, int buf, int first_row) {
+  // ---- per-lane constants: the row / 16-byte chunk of a step that each
+  // vector of the staged loads holds, and where it goes in the rings ----
+  int kgoff[C::kKVec], kgrow[C::kKVec], vgoff[C::kVVec], vgrow[C::kVVec];
+  unsigned char *kwp[C::kKVec], *vwp[C::kVVec];
 #pragma unroll
-    for (int x = 0; x < C::kVec; ++x) {
-      const int u = x * 64 + lane;
-      const int row = u / C::kChunks, ch = u % C::kChunks;
-      const int tok = w0 + step * C::kStep + row;
-      const uint32_t off = row >= first_row ? (uint32_t)(tok * D + ch * 8) * 2u : kOutOfRange;
-      stage[buf][0][x] = bload16(rk, off);
-      stage[buf][1][x] = bload16(rv, off);
-    }
-  };
-  auto commit = [&](int step, int buf) {
-    const int slot = (step + C::kSlots) % C::kSlots;
+  for (int x = 0; x < C::kKVec; ++x) {
+    const int u = x * 64 + lane;
+    const int row = u / C::kKChunks, ch = u % C::kKChunks;
+    kgrow[x] = row;
+    kgoff[x] = ((w0 + row) * D + 32 * kh + ch * 8) * 2;
+    kwp[x] = ring + row * C::kKRow + ((ch ^ (row & (C::kKChunks - 1))) << 4);
+  }
 #pragma unroll
-    for (int x = 0; x < C::kVec; ++x) {
-      const int u = x * 64 + lane;
-      const int row = u / C::kChunks, ch = u % C::kChunks;
-      const int off = row * C::kRowBytes + ((ch ^ (row & (C::kChunks - 1))) << 4);
-#pragma unroll
-      for (int tn = 0; tn < 2; ++tn)
-        *reinterpret_cast<u32x4_t*>(ring + (tn * C::kSlots + slot) * C::kSlotBytes + off) =
-            stage[buf][tn][x];
-    }
-  };
+  for (int x = 0; x < C::kVVec; ++x) {
+    const int u = x * 64 + lane;
+    const int row = u / C::kVChunks, ch = u % C::kVChunks;
+    vgrow[x] = row;
+    vgoff[x] = ((w0 + row) * D + ch * 8) * 2;
+    vwp[x] = ring + C::kKRing + row * C::kVRow + ((ch ^ (row & (C::kVChunks - 1))) << 4);
+  }
 
-  // Only rows 12..15 of the step before the wave's first token are needed
-  // (the conv window); the others are masked off.
-  issue(-1, 1, nsteps > 0 ? C::kStep - 4 : C::kStep);
-  issue(0, 0, nsteps > 0 ? 0 : C::kStep);
+  u32x4_t sk[2][C::kKVec], sv[2][C::kVVec];  // [in-flight buffer = step % 2][vector]
+  auto issue = [&](int step, int buf, bool live) {
+#pragma unroll
+    for (int x = 0; x < C::kKVec; ++x)
+      sk[buf][x] = bload16(rk, live ? (uint32_t)(kgoff[x] + step * C::kStepBytes) : kOutOfRange);
+#pragma unroll
+    for (int x = 0; x < C::kVVec; ++x)
+      sv[buf][x] = bload16(rv, live ? (uint32_t)(vgoff[x] + step * C::kStepBytes) : kOutOfRange);
+  };
+  auto commit = [&](int slot, int buf) {
+#pragma unroll
+    for (int x = 0; x < C::kKVec; ++x)
+      *reinterpret_cast<u32x4_t*>(kwp[x] + slot * C::kKSlot) = sk[buf][x];
+#pragma unroll
+    for (int x = 0; x < C::kVVec; ++x)
+      *reinterpret_cast<u32x4_t*>(vwp[x] + slot * C::kVSlot) = sv[buf][x];
+  };
+  // Of the step before the part's first token only rows 12..15 (the conv
+  // window) are needed; they sit in the vectors from kXk / kXv on.
+  constexpr int kXk = 12 * C::kKChunks / 64, kXv = 12 * C::kVChunks / 64;
+  u32x4_t mk[C::kKVec - kXk], mv[C::kVVec - kXv];
+#pragma unroll
+  for (int x = kXk; x < C::kKVec; ++x)
+    mk[x - kXk] = bload16(rk, kgrow[x] >= C::kStep - 4 && nsteps > 0
+                                  ? (uint32_t)(kgoff[x] - C::kStepBytes) : kOutOfRange);
+#pragma unroll
+  for (int x = kXv; x < C::kVVec; ++x)
+    mv[x - kXv] = bload16(rv, vgrow[x] >= C::kStep - 4 && nsteps > 0
+                                  ? (uint32_t)(vgoff[x] - C::kStepBytes) : kOutOfRange);
+  issue(0, 0, nsteps > 0);
+  issue(1, 1, nsteps > 1);
+  // Keep every load above in flight before any of the work below: the
+  // scheduler would otherwise hoist the gate pass (and its wait for the
+  // logits) ahead of the prefetches.
+  __builtin_amdgcn_sched_barrier(0);
 
-  // ---- gate weights of the wave's tokens: m_w, w_j = exp(a_j - m_w), l_w ----
+  // ---- gate weights of the part's tokens: m_w, w_j = exp(a_j - m_w), l_w ----
   float av[C::kMaxQ / 64];
   float mloc = -INFINITY;
 #pragma unroll
   for (int i = 0; i < C::kMaxQ / 64; ++i) {
-    const int tok = w0 + lane + 64 * i;
-    av[i] = (64 * i < Q && tok < w1) ? __uint_as_float(abits[i] << 16) : -INFINITY;
+    av[i] = __uint_as_float(abits[i] << 16) + amask[i];
     mloc = fmaxf(mloc, av[i]);
   }
-  const float mw = wave_max(mloc);
+  const float mw = __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(
+                                              __builtin_bit_cast(int, wave_max(mloc))));
   float lsum = 0.0f;
 #pragma unroll
   for (int i = 0; i < C::kMaxQ / 64; ++i) {
-    if (64 * i < Q) {
-      const float wv = av[i] == -INFINITY ? 0.0f : __expf(av[i] - mw);
-      wbuf[lane + 64 * i] = wv;
-      lsum += wv;
-    }
+    // every entry is written: the padded steps of the last turn read zeros
+    const float wv = av[i] == -INFINITY ? 0.0f : __expf(av[i] - mw);
+    wbuf[lane + 64 * i] = wv;
+    lsum += wv;
   }
-  const float lw = wave_sum(lsum);
+  const float lw = __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(
+                                              __builtin_bit_cast(int, wave_sum(lsum))));
 
-  f32x16_t acc[kT][kT];
+  f32x16_t acc[4][kTB];  // M_tau restricted to the wave's 32 key channels
 #pragma unroll
-  for (int a = 0; a < kT; ++a)
+  for (int u = 0; u < 4; ++u)
 #pragma unroll
-    for (int b = 0; b < kT; ++b)
+    for (int b = 0; b < kTB; ++b)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) acc[a][b][i] = 0.0f;
-  float zacc[kT];
+      for (int i = 0; i < 16; ++i) acc[u][b][i] = 0.0f;
+  float zacc = 0.0f;
 #pragma unroll
-  for (int t = 0; t < kT; ++t) zacc[t] = 0.0f;
+  for (int tap = 0; tap < 4; ++tap) wk[tap] *= kLog2e;
 
-  commit(-1, 1);
-  issue(1, 1, nsteps > 1 ? 0 : C::kStep);
-  commit(0, 0);
-  issue(2, 0, nsteps > 2 ? 0 : C::kStep);
-
-  // Lane roles for the transposed reads and the MFMA operands.
-  const int half = lane >> 5;             // token half of the 16-token step
+  // Lane roles for the transposed reads and the MFMA operands.  Read r hands
+  // the lane rows 8*half - 4 + 4r + [0, 4) of one channel (key channel kch,
+  // value channel 32b + (lane & 31)); rows before 0 are rows 12..15 of the
+  // previous slot.
+  const int half = lane >> 5;  // token half of the 16-token step
   const int grp_ch = 16 * ((lane >> 4) & 1);
   const int j = lane & 15;
   const int src_row = j >> 2, src_ch = 4 * (j & 3);
+  const int row0 = 8 * half - 4 + src_row;
+  const bool prv = row0 < 0;
+  const int rr0 = prv ? row0 + C::kStep : row0;
+  // [read 0 for slots >= 1, read 0 for slot 0, read 1, read 2]
+  const unsigned char* kp[4];
+  const unsigned char* vp[kTB][4];
+  {
+    const int e0 = grp_ch + src_ch;
+    const int o0 = swz<C::kKChunks>(rr0, e0);
+    kp[0] = ring + o0 - (prv ? C::kKSlot : 0);
+    kp[1] = ring + o0 + (prv ? (C::kSlots - 1) * C::kKSlot : 0);
+    kp[2] = ring + swz<C::kKChunks>(row0 + 4, e0);
+    kp[3] = ring + swz<C::kKChunks>(row0 + 8, e0);
+  }
+#pragma unroll
+  for (int b = 0; b < kTB; ++b) {
+    const int e0 = 32 * b + grp_ch + src_ch;
+    const unsigned char* vr = ring + C::kKRing;
+    const int o0 = swz<C::kVChunks>(rr0, e0);
+    vp[b][0] = vr + o0 - (prv ? C::kVSlot : 0);
+    vp[b][1] = vr + o0 + (prv ? (C::kSlots - 1) * C::kVSlot : 0);
+    vp[b][2] = vr + swz<C::kVChunks>(row0 + 4, e0);
+    vp[b][3] = vr + swz<C::kVChunks>(row0 + 8, e0);
+  }
+  const float* wl = wbuf + 8 * half;
 
-  auto step_body = [&](int i, auto nb) {
-    constexpr int kNext = decltype(nb)::value;  // staging buffer of step i+1
-    const unsigned char* kcur = ring + (0 * C::kSlots + i % C::kSlots) * C::kSlotBytes;
-    const unsigned char* kprv = ring + (0 * C::kSlots + (i + C::kSlots - 1) % C::kSlots) * C::kSlotBytes;
-    const unsigned char* vcur = ring + (1 * C::kSlots + i % C::kSlots) * C::kSlotBytes;
-    const unsigned char* vprv = ring + (1 * C::kSlots + (i + C::kSlots - 1) % C::kSlots) * C::kSlotBytes;
-    // gate weights of the lane's eight tokens
-    const f32x4_t wa = *reinterpret_cast<const f32x4_t*>(wbuf + 16 * i + 8 * half);
-    const f32x4_t wb = *reinterpret_cast<const f32x4_t*>(wbuf + 16 * i + 8 * half + 4);
-    const float wj[8] = {wa[0], wa[1], wa[2], wa[3], wb[0], wb[1], wb[2], wb[3]};
-
-    u32x4_t A[kT], Bh[kT], Bl[kT];
+  // One step: transposed reads of the twelve-row windows (dword m of read r
+  // holds rows 8*half - 4 + 4r + 2m', +1), the operands, the products.
+  auto step = [&](auto slot_c, int i) {
+    constexpr int sl = decltype(slot_c)::value;
+    u32x2_t wkr[3], wvr[kTB][3];
 #pragma unroll
-    for (int t = 0; t < kT; ++t) {
-      const int e0 = 32 * t + grp_ch + src_ch;
-      float xk[12], xv[12];
-#pragma unroll
-      for (int r = 0; r < 3; ++r) {
-        const int row = 8 * half + 4 * r - 4 + src_row;  // -4 .. 15
-        const unsigned char* kb = row < 0 ? kprv : kcur;
-        const unsigned char* vb = row < 0 ? vprv : vcur;
-        const int rr = row < 0 ? row + 16 : row;
-        const i16x4_t qk = tr_read(kb + swz<D>(rr, e0));
-        const i16x4_t qv = tr_read(vb + swz<D>(rr, e0));
-        const u32x2_t uk = __builtin_bit_cast(u32x2_t, qk);
-        const u32x2_t uv = __builtin_bit_cast(u32x2_t, qv);
-        xk[4 * r + 0] = bf16_lo(uk[0]); xk[4 * r + 1] = bf16_hi(uk[0]);
-        xk[4 * r + 2] = bf16_lo(uk[1]); xk[4 * r + 3] = bf16_hi(uk[1]);
-        xv[4 * r + 0] = bf16_lo(uv[0]); xv[4 * r + 1] = bf16_hi(uv[0]);
-        xv[4 * r + 2] = bf16_lo(uv[1]); xv[4 * r + 3] = bf16_hi(uv[1]);
-      }
-      float kw[8], vt[8];
-#pragma unroll
-      for (int o = 0; o < 8; ++o) {
-        float kc = wk[t][0] * xk[o + 1];
-        float vc = wvt[t][0] * xv[o + 1];
-#pragma unroll
-        for (int tap = 1; tap < 4; ++tap) {
-          kc = fmaf(wk[t][tap], xk[o + 1 + tap], kc);
-          vc = fmaf(wvt[t][tap], xv[o + 1 + tap], vc);
-        }
-        const float ph = fmaxf(kc, 0.0f) + __expf(fminf(kc, 0.0f));
-        kw[o] = wj[o] * ph;
-        zacc[t] += kw[o];
-        vt[o] = vc;
-      }
-#pragma unroll
-      for (int p = 0; p < 4; ++p) {
-        A[t][p] = pack_bf16x2(kw[2 * p], kw[2 * p + 1]);
-        const uint32_t hi = pack_bf16x2(vt[2 * p], vt[2 * p + 1]);
-        Bh[t][p] = hi;
-        Bl[t][p] = pack_bf16x2(vt[2 * p] - bf16_lo(hi), vt[2 * p + 1] - bf16_hi(hi));
-      }
+    for (int r = 0; r < 3; ++r) {
+      const unsigned char* b = (r == 0 ? (sl == 0 ? kp[1] : kp[0]) : kp[r + 1]) + sl * C::kKSlot;
+      wkr[r] = __builtin_bit_cast(u32x2_t, tr_read(b));
     }
 #pragma unroll
-    for (int a = 0; a < kT; ++a)
+    for (int bt = 0; bt < kTB; ++bt)
 #pragma unroll
-      for (int b = 0; b < kT; ++b) {
-        acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-            __builtin_bit_cast(bf16x8_t, A[a]), __builtin_bit_cast(bf16x8_t, Bh[b]), acc[a][b], 0, 0, 0);
-        acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-            __builtin_bit_cast(bf16x8_t, A[a]), __builtin_bit_cast(bf16x8_t, Bl[b]), acc[a][b], 0, 0, 0);
+      for (int r = 0; r < 3; ++r) {
+        const unsigned char* b = (r == 0 ? (sl == 0 ? vp[bt][1] : vp[bt][0]) : vp[bt][r + 1]) + sl * C::kVSlot;
+        wvr[bt][r] = __builtin_bit_cast(u32x2_t, tr_read(b));
       }
-    // Stage step i+1 into the ring (its slot held step i-3) and refill the
-    // freed registers with step i+3.  Both run unconditionally so the wait
-    // counts are the same on every path; steps past the end are loaded with
-    // every row out of range (no memory traffic, zeros).
-    commit(i + 1, kNext);
-    issue(i + 3, kNext, i + 3 < nsteps ? 0 : C::kStep);
+    // gate weights of the lane's eight tokens
+    const f32x4_t wa = *reinterpret_cast<const f32x4_t*>(wl + 16 * i);
+    const f32x4_t wb = *reinterpret_cast<const f32x4_t*>(wl + 16 * i + 4);
+    const float wj[8] = {wa[0], wa[1], wa[2], wa[3], wb[0], wb[1], wb[2], wb[3]};
+    // A = w phi(kt) of key channel kch over the lane's eight tokens
+    float xk[12];
+#pragma unroll
+    for (int r = 0; r < 3; ++r) {
+      xk[4 * r + 0] = bf16_lo(wkr[r][0]); xk[4 * r + 1] = bf16_hi(wkr[r][0]);
+      xk[4 * r + 2] = bf16_lo(wkr[r][1]); xk[4 * r + 3] = bf16_hi(wkr[r][1]);
+    }
+    float kw[8];
+#pragma unroll
+    for (int o = 0; o < 8; ++o) {
+      float kc = wk[0] * xk[o + 1];  // kt * log2(e)
+#pragma unroll
+      for (int tap = 1; tap < 4; ++tap) kc = fmaf(wk[tap], xk[o + 1 + tap], kc);
+      // phi(x) = max(x, 0) + exp(min(x, 0)) = ln2 max(x', 0) + 2^min(x', 0)
+      const float ph = fmaf(kLn2, fmaxf(kc, 0.0f), __builtin_amdgcn_exp2f(fminf(kc, 0.0f)));
+      kw[o] = wj[o] * ph;
+      zacc += kw[o];
+    }
+    u32x4_t A;
+#pragma unroll
+    for (int p = 0; p < 4; ++p) A[p] = pack_bf16x2(kw[2 * p], kw[2 * p + 1]);
+    // B[tau] = value rows of the lane's eight tokens shifted by tau - 3: the
+    // window starts at row tau + 1 (odd shifts straddle two dwords)
+#pragma unroll
+    for (int bt = 0; bt < kTB; ++bt) {
+      const uint32_t pv[6] = {wvr[bt][0][0], wvr[bt][0][1], wvr[bt][1][0],
+                              wvr[bt][1][1], wvr[bt][2][0], wvr[bt][2][1]};
+      u32x4_t B[4];
+#pragma unroll
+      for (int m = 0; m < 4; ++m) {
+        B[0][m] = __builtin_amdgcn_alignbit(pv[m + 1], pv[m], 16);
+        B[1][m] = pv[m + 1];
+        B[2][m] = __builtin_amdgcn_alignbit(pv[m + 2], pv[m + 1], 16);
+        B[3][m] = pv[m + 2];
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        acc[u][bt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+            __builtin_bit_cast(bf16x8_t, A), __builtin_bit_cast(bf16x8_t, B[u]), acc[u][bt], 0, 0, 0);
+    }
   };
-  int i = 0;
-  for (; i + 1 < nsteps; i += 2) {
-    step_body(i, std::integral_constant<int, 1>{});
-    step_body(i + 1, std::integral_constant<int, 0>{});
-  }
-  if (i < nsteps) step_body(i, std::integral_constant<int, 1>{});
 
-  // ---- merge the four waves' partial states into the chunk's record ----
+  // Pipeline: at the top of step i, step i+1 is staged into its slot (the
+  // slot of step i-3) and its registers are refilled with step i+3; then
+  // step i is read back and computed.  The other wave on the SIMD covers the
+  // read latency and overlaps its vector work with these MFMAs.  Loads and
+  // stores run on every path, so the wait counts are the same everywhere;
+  // steps past the end load only out-of-range rows (no traffic, zeros).
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  using I2 = std::integral_constant<int, 2>;
+  using I3 = std::integral_constant<int, 3>;
 #pragma unroll
-  for (int t = 0; t < kT; ++t) zacc[t] += __shfl_xor(zacc[t], 32);
-  __syncthreads();  // every wave is done with its ring
-  float* Sw = reinterpret_cast<float*>(ring);
+  for (int x = kXk; x < C::kKVec; ++x)
+    *reinterpret_cast<u32x4_t*>(kwp[x] + (C::kSlots - 1) * C::kKSlot) = mk[x - kXk];
 #pragma unroll
-  for (int a = 0; a < kT; ++a)
-#pragma unroll
-    for (int b = 0; b < kT; ++b)
-#pragma unroll
-      for (int q = 0; q < 16; ++q) {
-        const int c = 32 * a + 8 * (q / 4) + 4 * half + (q % 4);
-        const int e = 32 * b + (lane & 31);
-        Sw[c * D + e] = acc[a][b][q];
-      }
-  float* zw = wbuf;  // reuse: z_w[D], m_w, l_w
-  if (lane < 32) {
-#pragma unroll
-    for (int t = 0; t < kT; ++t) zw[32 * t + lane] = zacc[t];
+  for (int x = kXv; x < C::kVVec; ++x)
+    *reinterpret_cast<u32x4_t*>(vwp[x] + (C::kSlots - 1) * C::kVSlot) = mv[x - kXv];
+  commit(0, 0);
+  issue(2, 0, nsteps > 2);
+  for (int it = 0; it < nturns; ++it) {
+    const int i = it * C::kSlots;
+    commit(1, 1);
+    issue(i + 3, 1, i + 3 < nsteps);
+    step(I0{}, i);
+    commit(2, 0);
+    issue(i + 4, 0, i + 4 < nsteps);
+    step(I1{}, i + 1);
+    commit(3, 1);
+    issue(i + 5, 1, i + 5 < nsteps);
+    step(I2{}, i + 2);
+    commit(0, 0);
+    issue(i + 6, 0, i + 6 < nsteps);
+    step(I3{}, i + 3);
   }
-  if (lane == 0) {
-    zw[D] = mw;
-    zw[D + 1] = lw;
+
+  // ---- merge: the waves of a part fill its D x D state, the parts are
+  // rescaled to the chunk maximum and summed in a fixed order ----
+  zacc += __shfl_xor(zacc, 32);
+  __syncthreads();  // every wave is done with its rings
+  float* Sp = reinterpret_cast<float*>(lds) + part * C::kPartFloats;
+#pragma unroll
+  for (int b = 0; b < kTB; ++b) {
+    const int e = 32 * b + (lane & 31);  // the channel of wv[b]
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      const int c = 32 * kh + 8 * (q / 4) + 4 * half + (q % 4);
+      float sv = wv[b][0] * acc[0][b][q];
+#pragma unroll
+      for (int u = 1; u < 4; ++u) sv = fmaf(wv[b][u], acc[u][b][q], sv);
+      Sp[c * D + e] = sv;
+    }
+  }
+  if (lane < 32) Sp[D * D + kch] = zacc;
+  if (kh == 0 && lane == 0) {
+    Sp[D * D + D] = mw;
+    Sp[D * D + D + 1] = lw;
   }
   __syncthreads();
-  const float* wb0 = reinterpret_cast<const float*>(lds + C::kWaves * C::kWaveBytes);
-  float mws[C::kWaves], f[C::kWaves];
+  const float* S0 = reinterpret_cast<const float*>(lds);
+  float f[C::kParts];
   float M = -INFINITY;
 #pragma unroll
-  for (int w = 0; w < C::kWaves; ++w) {
-    mws[w] = wb0[w * C::kMaxQ + D];
-    M = fmaxf(M, mws[w]);
+  for (int p = 0; p < C::kParts; ++p) M = fmaxf(M, S0[p * C::kPartFloats + D * D + D]);
+#pragma unroll
+  for (int p = 0; p < C::kParts; ++p) {
+    const float mp = S0[p * C::kPartFloats + D * D + D];
+    f[p] = mp == -INFINITY ? 0.0f : __expf(mp - M);
   }
-#pragma unroll
-  for (int w = 0; w < C::kWaves; ++w) f[w] = mws[w] == -INFINITY ? 0.0f : __expf(mws[w] - M);
-#pragma unroll
-  for (int k = 0; k < D * D / C::kNT; ++k) {
-    const int x = k * C::kNT + tid;
+  for (int x = tid; x < D * D + D; x += C::kNT) {
     float v = 0.0f;
 #pragma unroll
-    for (int w = 0; w < C::kWaves; ++w)
-      v = fmaf(f[w], reinterpret_cast<const float*>(lds + w * C::kWaveBytes)[x], v);
+    for (int p = 0; p < C::kParts; ++p) v = fmaf(f[p], S0[p * C::kPartFloats + x], v);
     rec[x] = v;
-  }
-  if (tid < D) {
-    float v = 0.0f;
-#pragma unroll
-    for (int w = 0; w < C::kWaves; ++w) v = fmaf(f[w], wb0[w * C::kMaxQ + tid], v);
-    rec[D * D + tid] = v;
   }
   if (tid == 0) {
     float l = 0.0f;
 #pragma unroll
-    for (int w = 0; w < C::kWaves; ++w) l = fmaf(f[w], wb0[w * C::kMaxQ + D + 1], l);
+    for (int p = 0; p < C::kParts; ++p) l = fmaf(f[p], S0[p * C::kPartFloats + D * D + D + 1], l);
     rec[D * D + D] = M;
     rec[D * D + D + 1] = l;
   }
@@ -543,7 +629,8 @@ bool stream_supported(const Plan& p) {
   // Every (sequence, head) slice must stay below 2^31 bytes for the 32-bit
   // buffer offsets; the fp32 output rows are the widest.
   return p.dtype == GBLA_BF16 && (p.d == 32 || p.d == 64) &&
-         p.chunk <= SS<64>::kWaves * SS<64>::kMaxQ && p.chunk % (16 * SS<64>::kWaves) == 0 &&
+         p.chunk <= SS<64>::kMaxChunk && p.chunk % (SS<32>::kStep * SS<32>::kParts) == 0 &&
+         p.chunk % (SS<64>::kStep * SS<64>::kParts) == 0 &&
          p.rtile % 128 == 0 && (int64_t)p.rows * p.d * 4 < (int64_t(1) << 31);
 }
 
