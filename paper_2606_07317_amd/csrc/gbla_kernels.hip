@@ -423,23 +423,21 @@ __device__ __forceinline__ void frag_put(void* frag_sh, int mb, int kb, int lane
   }
 }
 
-// grid = (N * H, element slices of 64).  Thread (x, pg) of a block sums the
-// element x of partials pg, pg + 4, ... (in that order) scaled by
-// exp(m_p - M); the four sums are added in the order pg = 0..3, then divided
-// by Z = sum_p exp(m_p - M) l_p.  The partials are taken in rounds of 32:
-// every load of a round (m_p, l_p and element x of the thread's eight
-// partials) is issued at once, and a later round with a larger maximum
-// rescales what came before.  The split of the partials is a function of
-// the shape only, so the result is the same on every call.
-template <typename T, int D>
+// grid = (N * H, element slices of kThreads * E).  A block stages the chunk
+// weights w_p = exp(m_p - M) of its (sequence, head) in LDS and forms
+// Z = sum_p w_p l_p; each thread then sums element x of every partial in the
+// order p = 0, 1, ..., scales by 1/Z and writes S, z and the readout
+// fragments.  Every reduction order is fixed by the shape alone (not by E or
+// the grid), so every call gives the same bits.
+constexpr int kCombineStage = 1024;  // chunk weights staged in LDS per round
+
+template <typename T, int D, int E>
 __global__ void __launch_bounds__(kThreads)
 combine_kernel(Plan P, const int32_t* __restrict__ cu, const float* __restrict__ partials,
                float* __restrict__ S_out, float* __restrict__ z_out, unsigned char* __restrict__ frags) {
   constexpr int kElems = D * D + D;
-  constexpr int kPer = 8;               // partials per thread per round
-  constexpr int kRound = 4 * kPer;      // partials per round
-  __shared__ float red[4];
-  __shared__ float part[4][64];
+  __shared__ float red[kThreads / 64];
+  __shared__ float wst[kCombineStage];
   const int tid = threadIdx.x;
   const int sh_idx = blockIdx.x;
   const int s = sh_idx / P.heads, h = sh_idx % P.heads;
@@ -451,72 +449,95 @@ combine_kernel(Plan P, const int32_t* __restrict__ cu, const float* __restrict__
     first = s * P.chunks_per_seq;
     count = P.chunks_per_seq;
   }
-  const float* recs = partials + ((size_t)h * P.units + first) * P.rec_floats;
-  const int xl = tid & 63, pg = tid >> 6;
-  const int x = blockIdx.y * 64 + xl;
-  const int xc = x < kElems ? x : 0;    // element read (a valid address for every lane)
-  const float xmask = x < kElems ? 1.0f : 0.0f;
+  const size_t rf = P.rec_floats;
+  const float* recs = partials + ((size_t)h * P.units + first) * rf;
 
-  float M = -INFINITY, zl = 0.0f, v = 0.0f;
-  for (int base = 0; base < count; base += kRound) {
-    float mv[kPer], lv[kPer], ev[kPer], pm[kPer];
-#pragma unroll
-    for (int j = 0; j < kPer; ++j) {
-      const int p = base + pg + 4 * j;
-      const float* r = recs + (size_t)(p < count ? p : 0) * P.rec_floats;
-      mv[j] = r[kElems];
-      lv[j] = r[kElems + 1];
-      ev[j] = r[xc];
-      pm[j] = p < count ? 0.0f : -INFINITY;  // added, not selected: the loads stay unconditional
-    }
-    float ml = -INFINITY;
-#pragma unroll
-    for (int j = 0; j < kPer; ++j) {
-      mv[j] += pm[j];
-      ml = fmaxf(ml, mv[j]);
-    }
-    const float Mr = block_max(ml, red);
-    const float Mn = fmaxf(M, Mr);
-    if (Mn != -INFINITY) {
-      const float f = M == -INFINITY ? 0.0f : gexp<T>(M - Mn);
-      zl *= f;
-      v *= f;
-#pragma unroll
-      for (int j = 0; j < kPer; ++j) {
-        const float w = mv[j] == -INFINITY ? 0.0f : gexp<T>(mv[j] - Mn);
-        zl = fmaf(w, lv[j], zl);
-        v = fmaf(w, ev[j], v);
+  // M = max_p m_p and Z = sum_p exp(m_p - M) l_p: thread t takes p = t,
+  // t + kThreads, ... in order; the waves' sums are added in wave order.
+  // With at most kThreads partials, thread t loads (m_t, l_t) once and the
+  // weights are staged from registers; the arithmetic is the same.
+  const bool one = count <= kThreads;
+  const int pc = tid < count ? tid : 0;
+  const float m1 = recs[pc * rf + kElems], l1 = recs[pc * rf + kElems + 1];
+  float ml = -INFINITY;
+  if (one) {
+    if (tid < count) ml = m1;
+  } else {
+    for (int p = tid; p < count; p += kThreads) ml = fmaxf(ml, recs[p * rf + kElems]);
+  }
+  const float M = block_max(ml, red);
+  float zl = 0.0f;
+  if (M != -INFINITY) {
+    if (one) {
+      if (tid < count) zl = gexp<T>(m1 - M) * l1;
+    } else {
+      for (int p = tid; p < count; p += kThreads) {
+        const float* r = recs + p * rf + kElems;
+        zl = fmaf(gexp<T>(r[0] - M), r[1], zl);
       }
     }
-    M = Mn;
   }
-  // Z over the four partial groups: every wave holds the same pg-group sum
-  // in each of its lanes, so lane 0 of each wave contributes once.
+  zl = wave_sum(zl);
   __syncthreads();
   if ((tid & 63) == 0) red[tid >> 6] = zl;
   __syncthreads();
-  const float Z = (red[0] + red[1]) + (red[2] + red[3]);
+  float Z = 0.0f;
+#pragma unroll
+  for (int w = 0; w < kThreads / 64; ++w) Z += red[w];
   const float invZ = Z > 0.0f ? 1.0f / Z : 0.0f;
-  part[pg][xl] = v * xmask;
-  __syncthreads();
-  if (tid >= 64 || x >= kElems) return;
-  const float val = (((part[0][xl] + part[1][xl]) + part[2][xl]) + part[3][xl]) * invZ;
+
+  int xe[E];
+  float v[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const int x = (blockIdx.y * E + e) * kThreads + tid;
+    xe[e] = x < kElems ? x : 0;  // a valid address for every thread
+    v[e] = 0.0f;
+  }
+  for (int p0 = 0; p0 < count; p0 += kCombineStage) {
+    const int n = min(kCombineStage, count - p0);
+    __syncthreads();
+    if (one) {
+      if (tid < n) wst[tid] = M == -INFINITY || m1 == -INFINITY ? 0.0f : gexp<T>(m1 - M);
+    } else {
+      for (int p = tid; p < n; p += kThreads) {
+        const float mp = recs[(p0 + p) * rf + kElems];
+        wst[p] = M == -INFINITY || mp == -INFINITY ? 0.0f : gexp<T>(mp - M);
+      }
+    }
+    __syncthreads();
+    // unrolled so that many partials' loads are in flight at once
+#pragma unroll 16
+    for (int p = 0; p < n; ++p) {
+      const float w = wst[p];
+      const float* r = recs + (p0 + p) * rf;
+#pragma unroll
+      for (int e = 0; e < E; ++e) v[e] = fmaf(w, r[xe[e]], v[e]);
+    }
+  }
 
   const size_t sh = (size_t)s * P.heads + h;
   unsigned char* fr = frags + sh * P.frag_bytes;
-  if (x < D * D) {
-    const int c = x / D, e = x % D;
-    if (S_out) S_out[sh * D * D + x] = val;
-    const int kb = c / 32, gq = (c % 32) / 8, j = c % 8;
-    const int mb = 2 * (e / 32) + (e % 8) / 4, m = 4 * ((e % 32) / 8) + e % 4;
-    frag_put<T, D>(fr, mb, kb, 16 * gq + m, j, val);
-  } else {
-    const int c = x - D * D;
-    if (z_out) z_out[sh * D + c] = val;
-    const int kb = c / 32, gq = (c % 32) / 8, j = c % 8;
-    for (int m = 0; m < 16; ++m) frag_put<T, D>(fr, D / 16, kb, 16 * gq + m, j, val);
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const int x = (blockIdx.y * E + e) * kThreads + tid;
+    if (x >= kElems) continue;
+    const float val = v[e] * invZ;
+    if (x < D * D) {
+      const int c = x / D, ee = x % D;
+      if (S_out) S_out[sh * D * D + x] = val;
+      const int kb = c / 32, gq = (c % 32) / 8, j = c % 8;
+      const int mb = 2 * (ee / 32) + (ee % 8) / 4, m = 4 * ((ee % 32) / 8) + ee % 4;
+      frag_put<T, D>(fr, mb, kb, 16 * gq + m, j, val);
+    } else {
+      const int c = x - D * D;
+      if (z_out) z_out[sh * D + c] = val;
+      const int kb = c / 32, gq = (c % 32) / 8, j = c % 8;
+      for (int m = 0; m < 16; ++m) frag_put<T, D>(fr, D / 16, kb, 16 * gq + m, j, val);
+    }
   }
 }
+
 
 // ---------------------------------------------------------------------------
 // readout_kernel: grid = (readout units per head, H).
@@ -799,10 +820,19 @@ struct StateRun {
       e = last_launch_status();
     }
     if (e != GBLA_OK) return e;
+    // One element per thread while the grid stays small; four once there are
+    // many (sequence, head) pairs.  The result does not depend on the choice.
     constexpr int kElems = D * D + D;
-    const int slices = (kElems + 63) / 64;
-    hipLaunchKernelGGL((combine_kernel<T, D>), dim3(p.nseq * p.heads, slices), dim3(kThreads), 0,
-                       st, p, cu, (const float*)partials, S, z, base + p.off_frags);
+    const int64_t pairs = (int64_t)p.nseq * p.heads;
+    const int slices1 = (kElems + kThreads - 1) / kThreads;
+    if (pairs * slices1 <= 4096) {
+      hipLaunchKernelGGL((combine_kernel<T, D, 1>), dim3(pairs, slices1), dim3(kThreads), 0,
+                         st, p, cu, (const float*)partials, S, z, base + p.off_frags);
+    } else {
+      const int slices4 = (kElems + 4 * kThreads - 1) / (4 * kThreads);
+      hipLaunchKernelGGL((combine_kernel<T, D, 4>), dim3(pairs, slices4), dim3(kThreads), 0,
+                         st, p, cu, (const float*)partials, S, z, base + p.off_frags);
+    }
     return last_launch_status();
   }
 };

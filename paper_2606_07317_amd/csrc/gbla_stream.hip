@@ -6,13 +6,15 @@
 // form K^T V and K^T 1 with K = g (.) phi(K)):
 //     S_p = sum_j w_j phi(kt_j) vt_j^T,  z_p = sum_j w_j phi(kt_j),
 //     w_j = exp(a_j - m_p),  m_p = max_j a_j,  l_p = sum_j w_j.
-// The chunk is split into token parts; the two waves of a part share its
-// tokens and split the key channels (one 32-channel MFMA tile each), so two
-// waves run on every SIMD and each one's vector work overlaps the other's
-// MFMAs.  A wave streams its tokens 16 at a time: raw bf16 key (its 32
-// channels) and value rows are loaded two steps ahead into registers,
-// written row-major into the wave's LDS rings (16-byte chunks XOR-swizzled
-// by row), and read back with ds_read_b64_tr_b16, which hands each lane four
+// The chunk is split into token parts; the waves of a part share its tokens
+// and split the key channels (one 32-channel MFMA tile each) and, at
+// d = 128, the value channels into halves.  Every wave then holds at most
+// 128 accumulators, so two waves run on every SIMD and each one's vector
+// work overlaps the other's MFMAs.  A wave streams its tokens 16 at a time:
+// raw bf16 key (its 32 channels) and value (its channels) rows are loaded
+// two steps ahead into registers, written row-major into the wave's LDS
+// rings (16-byte chunks XOR-swizzled by row), and read back with
+// ds_read_b64_tr_b16, which hands each lane four
 // consecutive tokens of one channel.  Twelve key tokens (three reads) give
 // the lane the causal conv window of its eight tokens, so the key conv, phi
 // and the gate weight are applied in registers and the results are already
@@ -56,14 +58,19 @@ __device__ __forceinline__ i16x4_t tr_read(const unsigned char* p) {
 template <int D>
 struct SS {
   static constexpr int kStep = 16;                       // tokens per MFMA K block
-  static constexpr int kKH = D / 32;                      // waves sharing a token part
-  static constexpr int kWaves = 8;                        // two per SIMD
+  // The waves of a token part split the key channels into 32-channel tiles
+  // and, at d = 128, the value channels into halves, so that every wave holds
+  // at most 128 accumulators and two waves run on each SIMD.
+  static constexpr int kKH = D / 32;                      // key tiles
+  static constexpr int kVH = D == 128 ? 2 : 1;            // value slices
+  static constexpr int kVD = D / kVH;                     // value channels per wave
+  static constexpr int kWaves = 8;
   static constexpr int kNT = 64 * kWaves;
-  static constexpr int kParts = kWaves / kKH;             // token parts of a chunk
-  static constexpr int kTB = D / 32;                      // 32-wide value tiles
+  static constexpr int kParts = kWaves / (kKH * kVH);     // token parts of a chunk
+  static constexpr int kTB = kVD / 32;                    // 32-wide value tiles per wave
   static constexpr int kStepBytes = kStep * 2 * D;        // one step of rows in memory
   static constexpr int kKRow = 64;                        // a wave's 32 key channels of a row
-  static constexpr int kVRow = 2 * D;                     // a value row
+  static constexpr int kVRow = 2 * kVD;                   // a wave's value channels of a row
   static constexpr int kKChunks = kKRow / 16, kVChunks = kVRow / 16;
   static constexpr int kKSlot = kStep * kKRow, kVSlot = kStep * kVRow;
   static constexpr int kKVec = kKSlot / 1024, kVVec = kVSlot / 1024;  // 16-byte vectors per lane
@@ -75,7 +82,7 @@ struct SS {
   static constexpr int kPartFloats = D * D + D + 2;       // S, z, m, l of a part
   static constexpr int kMerge = kParts * kPartFloats * 4;
   static constexpr int kRings = kWaves * kRing > kMerge ? kWaves * kRing : kMerge;
-  static constexpr int kLds = kRings + kWaves * kMaxQ * 4;
+  static constexpr int kLds = kRings + kParts * kMaxQ * 4;  // + gate weights per part
 };
 
 // Byte offset of element e (a multiple of 4) of row r of a slot whose rows
@@ -96,7 +103,9 @@ state_stream_kernel(Plan P, const uint16_t* __restrict__ kin, const uint16_t* __
   __shared__ __attribute__((aligned(16))) unsigned char lds[C::kLds];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int part = wave / C::kKH, kh = wave % C::kKH;
+  const int part = wave / (C::kKH * C::kVH);
+  const int kh = (wave / C::kVH) % C::kKH, vh = wave % C::kVH;
+  const int vc0 = vh * C::kVD;  // first value channel of the wave
   const int h = blockIdx.y, g = blockIdx.x;
   int s, chunk;
   if (!unit_of<C::kNT>(P, cu, P.chunk, P.chunks_per_seq, g, &s, &chunk)) return;
@@ -117,7 +126,9 @@ state_stream_kernel(Plan P, const uint16_t* __restrict__ kin, const uint16_t* __
   // only out-of-range rows and zero gate weights and add nothing.
   const int nturns = (nsteps + C::kSlots - 1) / C::kSlots;
   unsigned char* ring = lds + wave * C::kRing;  // [key slots][value slots]
-  float* wbuf = reinterpret_cast<float*>(lds + C::kRings) + wave * C::kMaxQ;
+  // gate weights of the part: every wave of the part writes the same values
+  // before it reads them, so no barrier is needed
+  float* wbuf = reinterpret_cast<float*>(lds + C::kRings) + part * C::kMaxQ;
 
   const __amdgpu_buffer_rsrc_t rk = make_rsrc(kin + base_row * D, (uint32_t)(len * 2 * D));
   const __amdgpu_buffer_rsrc_t rv = make_rsrc(vin + base_row * D, (uint32_t)(len * 2 * D));
@@ -132,7 +143,7 @@ state_stream_kernel(Plan P, const uint16_t* __restrict__ kin, const uint16_t* __
   float wk[4], wv[kTB][4];
   load_taps4(conv_w, P.heads, h, 1, D, P.W, kch, wk);
 #pragma unroll
-  for (int b = 0; b < kTB; ++b) load_taps4(conv_w, P.heads, h, 2, D, P.W, 32 * b + (lane & 31), wv[b]);
+  for (int b = 0; b < kTB; ++b) load_taps4(conv_w, P.heads, h, 2, D, P.W, vc0 + 32 * b + (lane & 31), wv[b]);
   // Gate logits of the part's tokens; tokens outside it read as zero and get
   // -inf added below (an add, not a select on the loaded value, so that the
   // loads stay ahead of the prefetches instead of being sunk into branches).
@@ -163,7 +174,7 @@ state_stream_kernel(Plan P, const uint16_t* __restrict__ kin, const uint16_t* __
     const int u = x * 64 + lane;
     const int row = u / C::kVChunks, ch = u % C::kVChunks;
     vgrow[x] = row;
-    vgoff[x] = ((w0 + row) * D + ch * 8) * 2;
+    vgoff[x] = ((w0 + row) * D + vc0 + ch * 8) * 2;
     vwp[x] = ring + C::kKRing + row * C::kVRow + ((ch ^ (row & (C::kVChunks - 1))) << 4);
   }
 
@@ -237,7 +248,7 @@ state_stream_kernel(Plan P, const uint16_t* __restrict__ kin, const uint16_t* __
 
   // Lane roles for the transposed reads and the MFMA operands.  Read r hands
   // the lane rows 8*half - 4 + 4r + [0, 4) of one channel (key channel kch,
-  // value channel 32b + (lane & 31)); rows before 0 are rows 12..15 of the
+  // value channel vc0 + 32b + (lane & 31)); rows before 0 are rows 12..15 of the
   // previous slot.
   const int half = lane >> 5;  // token half of the 16-token step
   const int grp_ch = 16 * ((lane >> 4) & 1);
@@ -373,7 +384,7 @@ state_stream_kernel(Plan P, const uint16_t* __restrict__ kin, const uint16_t* __
   float* Sp = reinterpret_cast<float*>(lds) + part * C::kPartFloats;
 #pragma unroll
   for (int b = 0; b < kTB; ++b) {
-    const int e = 32 * b + (lane & 31);  // the channel of wv[b]
+    const int e = vc0 + 32 * b + (lane & 31);  // the channel of wv[b]
 #pragma unroll
     for (int q = 0; q < 16; ++q) {
       const int c = 32 * kh + 8 * (q / 4) + 4 * half + (q % 4);
@@ -383,8 +394,8 @@ state_stream_kernel(Plan P, const uint16_t* __restrict__ kin, const uint16_t* __
       Sp[c * D + e] = sv;
     }
   }
-  if (lane < 32) Sp[D * D + kch] = zacc;
-  if (kh == 0 && lane == 0) {
+  if (vh == 0 && lane < 32) Sp[D * D + kch] = zacc;  // value slices repeat z, m, l
+  if (vh == 0 && kh == 0 && lane == 0) {
     Sp[D * D + D] = mw;
     Sp[D * D + D + 1] = lw;
   }
@@ -435,11 +446,12 @@ struct RS {
   static constexpr int kVec = kSlotBytes / 1024;        // 16-byte vectors per lane per group
   static constexpr int kSlots = 3;
   static constexpr int kNMB = D / 16 + 1, kNKB = D / 32;
+  static constexpr int kOcc = D == 128 ? 1 : 2;         // waves per SIMD (registers)
   static constexpr int kLds = 4 * kSlots * kSlotBytes;
 };
 
 template <int D>
-__global__ void __launch_bounds__(kThreads, 2)
+__global__ void __launch_bounds__(kThreads, RS<D>::kOcc)
 readout_stream_kernel(Plan P, const uint16_t* __restrict__ qin, const uint16_t* __restrict__ rin,
                       const float* __restrict__ conv_w, const float* __restrict__ gamma,
                       const int32_t* __restrict__ cu, const unsigned char* __restrict__ frags,
@@ -628,9 +640,10 @@ readout_stream_kernel(Plan P, const uint16_t* __restrict__ qin, const uint16_t* 
 bool stream_supported(const Plan& p) {
   // Every (sequence, head) slice must stay below 2^31 bytes for the 32-bit
   // buffer offsets; the fp32 output rows are the widest.
-  return p.dtype == GBLA_BF16 && (p.d == 32 || p.d == 64) &&
+  return p.dtype == GBLA_BF16 && (p.d == 32 || p.d == 64 || p.d == 128) &&
          p.chunk <= SS<64>::kMaxChunk && p.chunk % (SS<32>::kStep * SS<32>::kParts) == 0 &&
          p.chunk % (SS<64>::kStep * SS<64>::kParts) == 0 &&
+         p.chunk % (SS<128>::kStep * SS<128>::kParts) == 0 &&
          p.rtile % 128 == 0 && (int64_t)p.rows * p.d * 4 < (int64_t(1) << 31);
 }
 
@@ -638,7 +651,10 @@ gbla_status launch_state_stream(const Plan& p, const void* k, const void* v, con
                                 const float* conv_w, const int32_t* cu, float* partials,
                                 hipStream_t st) {
   const dim3 grid(p.units, p.heads);
-  if (p.d == 64)
+  if (p.d == 128)
+    hipLaunchKernelGGL((state_stream_kernel<128>), grid, dim3(SS<128>::kNT), 0, st, p,
+                       (const uint16_t*)k, (const uint16_t*)v, (const uint16_t*)a, conv_w, cu, partials);
+  else if (p.d == 64)
     hipLaunchKernelGGL((state_stream_kernel<64>), grid, dim3(SS<64>::kNT), 0, st, p,
                        (const uint16_t*)k, (const uint16_t*)v, (const uint16_t*)a, conv_w, cu, partials);
   else
@@ -651,7 +667,10 @@ gbla_status launch_readout_stream(const Plan& p, const void* q, const void* r, c
                                   const float* gamma, const int32_t* cu, const unsigned char* frags,
                                   float* out, hipStream_t st) {
   const dim3 grid(p.runits, p.heads);
-  if (p.d == 64)
+  if (p.d == 128)
+    hipLaunchKernelGGL((readout_stream_kernel<128>), grid, dim3(kThreads), 0, st, p,
+                       (const uint16_t*)q, (const uint16_t*)r, conv_w, gamma, cu, frags, out);
+  else if (p.d == 64)
     hipLaunchKernelGGL((readout_stream_kernel<64>), grid, dim3(kThreads), 0, st, p,
                        (const uint16_t*)q, (const uint16_t*)r, conv_w, gamma, cu, frags, out);
   else

@@ -70,6 +70,7 @@ SMALL_CASES = {
     "bf16_d64_n1000": small("b8_n2048_d64", batch=2, heads=3, seqlen=1000, seed=23),
     "bf16_d32_n3001_W2": small("b8_n2048_d64", batch=1, heads=2, seqlen=3001, head_dim=32, conv_width=2, seed=24),
     "bf16_d128_n777_W1": small("b8_n2048_d64", batch=2, heads=2, seqlen=777, head_dim=128, conv_width=1, seed=25),
+    "bf16_d128_n3000_W4": small("b8_n2048_d64", batch=1, heads=2, seqlen=3000, head_dim=128, seed=28),
     "bf16_d64_n1": small("b8_n2048_d64", batch=3, heads=2, seqlen=1, seed=26),
     "bf16_d64_n5": small("b8_n2048_d64", batch=2, heads=2, seqlen=5, seed=27),
 }
