@@ -60,6 +60,26 @@ typedef enum {
 
 typedef enum { GBLA_F32 = 0, GBLA_BF16 = 1 } gbla_dtype;
 
+/*
+ * Ablation switches, the rows of the paper's ablation table (Section 4,
+ * "Ablation"; "W/o Key gating", "W/o Conv1D", "W/o Gated RMSNorm", and all
+ * three, which is plain bidirectional linear attention, Eq. (1)).  OR them
+ * into shape->flags.  An input that a switch removes may be NULL and is
+ * ignored if given.
+ *   GBLA_NO_GATE  uniform key gates, g_j = 1/n over each sequence (the
+ *                 softmax of constant logits); gate_logits is not read.
+ *                 The scale cancels in o; gbla_state exports S and z with it.
+ *   GBLA_NO_CONV  identity Conv1D: qt = q, kt = k, vt = v; conv_w is not read.
+ *   GBLA_NO_NORM  out = o (no RMSNorm, gamma or SiLU gate); out_gate and
+ *                 norm_w are not read.
+ */
+enum {
+  GBLA_NO_GATE = 1,
+  GBLA_NO_CONV = 2,
+  GBLA_NO_NORM = 4,
+  GBLA_BLA = 7
+};
+
 typedef struct {
   int32_t batch;      /* B (dense) or N_s, the number of sequences (ragged)      */
   int32_t heads;      /* H >= 1                                                  */
@@ -69,6 +89,7 @@ typedef struct {
   int32_t max_seqlen; /* ragged: an upper bound of the lengths (>= 0); dense: 0  */
   int32_t dtype;      /* gbla_dtype of q, k, v, gate_logits and out_gate         */
   float eps;          /* RMSNorm epsilon, finite and >= 0                        */
+  uint32_t flags;     /* OR of GBLA_NO_* switches; 0 is the full GBLA layer      */
 } gbla_shape;
 
 /*
@@ -89,7 +110,9 @@ size_t gbla_workspace_bytes(const gbla_shape* shape);
  *   norm_w       [H,d] fp32, the RMSNorm weight gamma
  *   cu_seqlens   NULL (dense) or int32 [N_s + 1] (ragged)
  *   workspace    >= gbla_workspace_bytes(shape) bytes of device scratch
- *   out          [B,H,n,d] or [H,T,d] fp32, y
+ *   out          [B,H,n,d] or [H,T,d] fp32, y (o under GBLA_NO_NORM)
+ * gate_logits, conv_w and out_gate / norm_w may be NULL under the switch
+ * that removes them (see GBLA_NO_*).
  */
 gbla_status gbla_forward(const gbla_shape* shape, const void* q, const void* k,
                          const void* v, const void* gate_logits, const void* out_gate,

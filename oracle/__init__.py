@@ -106,13 +106,33 @@ class Oracle:
             raise ValueError("oracle rejected its arguments (code %d)" % rc)
         return outs
 
-    def forward_inputs(self, inp, want=("y",), nthreads: int = 0) -> dict:
-        """Run the oracle on a ``paper_2606_07317_amd.inputs.Inputs`` batch."""
+    def forward_inputs(self, inp, want=("y",), nthreads: int = 0, gate: bool = True,
+                       conv: bool = True, norm: bool = True) -> dict:
+        """Run the oracle on a ``paper_2606_07317_amd.inputs.Inputs`` batch.
+
+        ``gate``, ``conv`` and ``norm`` are the ablations of the paper's
+        ablation table (Section 4, "Ablation"), expressed through the inputs
+        so that the arithmetic above is unchanged:
+          gate=False  constant logits, hence uniform gates g_j = 1/n
+                      (Section 2.1, key gating; the softmax of a constant);
+          conv=False  identity taps (tap W-1 = 1, the others 0), so qt = q;
+          norm=False  the un-normalised readout o is returned as "y".
+        All three off is bidirectional linear attention, Eq. (1)."""
         w = inp.workload
-        return self.forward(inp.q, inp.k, inp.v, inp.a, inp.r, inp.conv_w, inp.gamma,
-                            nseq=inp.nseq, heads=w.heads, rows=inp.rows if inp.cu_seqlens is not None else w.seqlen,
-                            d=w.head_dim, W=w.conv_width, dtype=w.dtype, eps=inp.eps,
-                            cu_seqlens=inp.cu_seqlens, want=want, nthreads=nthreads)
+        a, conv_w = inp.a, inp.conv_w
+        if not gate:
+            a = np.zeros_like(inp.a)
+        if not conv:
+            conv_w = np.zeros_like(inp.conv_w)
+            conv_w[..., w.conv_width - 1] = 1.0
+        req = tuple(("o" if (x == "y" and not norm) else x) for x in want)
+        res = self.forward(inp.q, inp.k, inp.v, a, inp.r, conv_w, inp.gamma,
+                           nseq=inp.nseq, heads=w.heads, rows=inp.rows if inp.cu_seqlens is not None else w.seqlen,
+                           d=w.head_dim, W=w.conv_width, dtype=w.dtype, eps=inp.eps,
+                           cu_seqlens=inp.cu_seqlens, want=tuple(dict.fromkeys(req)), nthreads=nthreads)
+        if not norm and "y" in want:
+            res["y"] = res["o"]
+        return res
 
 
 _default: Optional[Oracle] = None

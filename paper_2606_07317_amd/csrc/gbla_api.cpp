@@ -37,6 +37,7 @@ gbla_status make_plan(const gbla_shape* s, bool ragged, Plan* p) {
   if (!(s->eps >= 0.0f) || !isfinite(s->eps)) return GBLA_ERR_INVALID_ARGUMENT;
   if (ragged && s->max_seqlen < 0) return GBLA_ERR_INVALID_ARGUMENT;
   if (s->heads > kMaxGridY) return GBLA_ERR_UNSUPPORTED;
+  if (s->flags & ~(uint32_t)GBLA_BLA) return GBLA_ERR_INVALID_ARGUMENT;
 
   Plan q{};
   q.nseq = s->batch;
@@ -47,6 +48,7 @@ gbla_status make_plan(const gbla_shape* s, bool ragged, Plan* p) {
   q.dtype = s->dtype;
   q.ragged = ragged ? 1 : 0;
   q.eps = s->eps;
+  q.flags = s->flags;
   q.tokens = ragged ? (int64_t)s->seqlen : (int64_t)s->batch * s->seqlen;
 
   // Chunk of the state reduction: about one workgroup per CU over all heads,
@@ -122,6 +124,22 @@ gbla_status check_logits(const Plan& p, const void* a) {
   return GBLA_OK;
 }
 
+// An input that the switch `flag` removes: NULL inside the library when the
+// switch is on (whatever the caller passed), otherwise the caller's pointer.
+template <typename Ptr>
+Ptr unless(const Plan& p, uint32_t flag, Ptr ptr) {
+  return (p.flags & flag) ? nullptr : ptr;
+}
+
+// Checks of the inputs that are in use: present and aligned.
+gbla_status check_used(std::initializer_list<const void*> used) {
+  for (const void* a : used) {
+    if (!a) return GBLA_ERR_INVALID_ARGUMENT;
+    if (!gbla::aligned(a, 16)) return GBLA_ERR_MISALIGNED;
+  }
+  return GBLA_OK;
+}
+
 #define GBLA_TRY(expr)                  \
   do {                                  \
     gbla_status _st = (expr);           \
@@ -147,8 +165,14 @@ gbla_status gbla_forward(const gbla_shape* shape, const void* q, const void* k, 
                          size_t workspace_bytes, float* out, void* stream) {
   Plan p;
   GBLA_TRY(gbla::make_plan(shape, cu_seqlens != nullptr, &p));
-  GBLA_TRY(check_acts(p, {q, k, v, out_gate, conv_w, norm_w, out}));
-  GBLA_TRY(check_logits(p, gate_logits));
+  gate_logits = unless(p, GBLA_NO_GATE, gate_logits);
+  conv_w = unless(p, GBLA_NO_CONV, conv_w);
+  out_gate = unless(p, GBLA_NO_NORM, out_gate);
+  norm_w = unless(p, GBLA_NO_NORM, norm_w);
+  GBLA_TRY(check_acts(p, {q, k, v, out}));
+  if (!(p.flags & GBLA_NO_CONV)) GBLA_TRY(check_used({conv_w}));
+  if (!(p.flags & GBLA_NO_NORM)) GBLA_TRY(check_used({out_gate, norm_w}));
+  if (!(p.flags & GBLA_NO_GATE)) GBLA_TRY(check_logits(p, gate_logits));
   GBLA_TRY(check_ws(p, workspace, workspace_bytes));
   hipStream_t st = static_cast<hipStream_t>(stream);
   GBLA_TRY(gbla::launch_state(p, k, v, gate_logits, conv_w, cu_seqlens, workspace, nullptr,
@@ -161,7 +185,9 @@ gbla_status gbla_conv1d(const gbla_shape* shape, const void* q, const void* k, c
                         float* v_t, void* stream) {
   Plan p;
   GBLA_TRY(gbla::make_plan(shape, cu_seqlens != nullptr, &p));
-  GBLA_TRY(check_acts(p, {q, k, v, conv_w, q_t, k_t, v_t}));
+  conv_w = unless(p, GBLA_NO_CONV, conv_w);
+  GBLA_TRY(check_acts(p, {q, k, v, q_t, k_t, v_t}));
+  if (!(p.flags & GBLA_NO_CONV)) GBLA_TRY(check_used({conv_w}));
   return gbla::launch_conv(p, q, k, v, conv_w, cu_seqlens, q_t, k_t, v_t,
                            static_cast<hipStream_t>(stream));
 }
@@ -172,8 +198,11 @@ gbla_status gbla_state(const gbla_shape* shape, const void* k, const void* v,
                        void* stream) {
   Plan p;
   GBLA_TRY(gbla::make_plan(shape, cu_seqlens != nullptr, &p));
-  GBLA_TRY(check_acts(p, {k, v, conv_w, S, z}));
-  GBLA_TRY(check_logits(p, gate_logits));
+  gate_logits = unless(p, GBLA_NO_GATE, gate_logits);
+  conv_w = unless(p, GBLA_NO_CONV, conv_w);
+  GBLA_TRY(check_acts(p, {k, v, S, z}));
+  if (!(p.flags & GBLA_NO_CONV)) GBLA_TRY(check_used({conv_w}));
+  if (!(p.flags & GBLA_NO_GATE)) GBLA_TRY(check_logits(p, gate_logits));
   GBLA_TRY(check_ws(p, workspace, workspace_bytes));
   return gbla::launch_state(p, k, v, gate_logits, conv_w, cu_seqlens, workspace, S, z,
                             static_cast<hipStream_t>(stream));
@@ -184,7 +213,12 @@ gbla_status gbla_readout(const gbla_shape* shape, const void* q, const void* out
                          void* workspace, size_t workspace_bytes, float* out, void* stream) {
   Plan p;
   GBLA_TRY(gbla::make_plan(shape, cu_seqlens != nullptr, &p));
-  GBLA_TRY(check_acts(p, {q, out_gate, conv_w, norm_w, out}));
+  conv_w = unless(p, GBLA_NO_CONV, conv_w);
+  out_gate = unless(p, GBLA_NO_NORM, out_gate);
+  norm_w = unless(p, GBLA_NO_NORM, norm_w);
+  GBLA_TRY(check_acts(p, {q, out}));
+  if (!(p.flags & GBLA_NO_CONV)) GBLA_TRY(check_used({conv_w}));
+  if (!(p.flags & GBLA_NO_NORM)) GBLA_TRY(check_used({out_gate, norm_w}));
   GBLA_TRY(check_ws(p, workspace, workspace_bytes));
   return gbla::launch_readout(p, q, out_gate, conv_w, norm_w, cu_seqlens, workspace, out,
                               static_cast<hipStream_t>(stream));

@@ -54,8 +54,14 @@ constexpr uint32_t kOutOfRange = 0x80000000u;
 
 // Taps of one tensor (0 = q, 1 = k, 2 = v), head h, channel c, right-aligned
 // to four taps: tap 3 multiplies the current token, taps before 4 - W are 0.
+// conv_w == NULL is the identity conv (the no-Conv1D switch).
 __device__ __forceinline__ void load_taps4(const float* conv_w, int H, int h, int tensor, int D,
                                            int W, int c, float* w4) {
+  if (conv_w == nullptr) {
+    w4[0] = w4[1] = w4[2] = 0.0f;
+    w4[3] = 1.0f;
+    return;
+  }
   const float* src = conv_w + (((size_t)tensor * H + h) * D + c) * W;
 #pragma unroll
   for (int t = 0; t < 4; ++t) {

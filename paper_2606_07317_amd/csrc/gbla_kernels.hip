@@ -48,6 +48,12 @@ __device__ __forceinline__ float load_scalar<uint16_t>(const uint16_t* p, int64_
   return __uint_as_float((uint32_t)p[i] << 16);
 }
 
+// Key-gate logit of token i; a == NULL (uniform gates) reads as 0.
+template <typename T>
+__device__ __forceinline__ float gate_logit(const T* a, int64_t i) {
+  return a ? load_scalar<T>(a, i) : 0.0f;
+}
+
 // Unpack the 16 bytes at one thread's slot: 8 bf16 or 4 fp32 channels.
 template <typename T>
 __device__ __forceinline__ void unpack16(const u32x4_t& u, float* x);
@@ -257,7 +263,7 @@ state_partial_kernel(Plan P, const T* __restrict__ kin, const T* __restrict__ vi
 
   // m_p: the chunk's largest gate logit.
   float mloc = -INFINITY;
-  for (int64_t t = t0 + tid; t < t1; t += kThreads) mloc = fmaxf(mloc, load_scalar<T>(ain, base_row + t));
+  for (int64_t t = t0 + tid; t < t1; t += kThreads) mloc = fmaxf(mloc, gate_logit<T>(ain, base_row + t));
   const float m = block_max(mloc, red);
 
   const int cg = tid % C::kCG, rg = tid / C::kCG;
@@ -309,7 +315,7 @@ state_partial_kernel(Plan P, const T* __restrict__ kin, const T* __restrict__ vi
       if (t < t1) {
         unpack16<T>(load16(kin + (base_row + t) * D + c0), xk[3 + j]);
         unpack16<T>(load16(vin + (base_row + t) * D + c0), xv[3 + j]);
-        wj[j] = gexp<T>(load_scalar<T>(ain, base_row + t) - m);
+        wj[j] = gexp<T>(gate_logit<T>(ain, base_row + t) - m);
       } else {
 #pragma unroll
         for (int c = 0; c < CPT; ++c) xk[3 + j][c] = xv[3 + j][c] = 0.0f;
@@ -641,7 +647,7 @@ readout_kernel(Plan P, const T* __restrict__ qin, const T* __restrict__ rin,
     for (int j = 0; j < 8; ++j) {
       const int c = 32 * kb + 8 * gq + j;
       load_taps4(conv_w, P.heads, h, 0, D, P.W, c, wq[kb][j]);
-      gm[kb][j] = gamma[(size_t)h * D + c];
+      gm[kb][j] = gamma ? gamma[(size_t)h * D + c] : 1.0f;
     }
 
   // Rows tb-3 .. tb-1 of the wave's first group, as lane 15 of a virtual
@@ -745,7 +751,15 @@ readout_kernel(Plan P, const T* __restrict__ qin, const T* __restrict__ rin,
       ss += __shfl_xor(ss, 32);
       const float scale = __builtin_amdgcn_rsqf(ss * (1.0f / D) + P.eps);
       const int64_t t = tb + 4 * n + j;
-      if (t < tt1) {
+      if (t < tt1 && !gamma) {  // out = o (no gated norm)
+        const int64_t row = base_row + t;
+#pragma unroll
+        for (int qq = 0; qq < NKB; ++qq) {
+          f32x4_t* dst = reinterpret_cast<f32x4_t*>(out + row * D + 32 * qq + 8 * gq);
+          dst[0] = acc[2 * qq];
+          dst[1] = acc[2 * qq + 1];
+        }
+      } else if (t < tt1) {
         const int64_t row = base_row + t;
 #pragma unroll
         for (int qq = 0; qq < NKB; ++qq) {

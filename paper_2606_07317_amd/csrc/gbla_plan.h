@@ -23,6 +23,7 @@ struct Plan {
   int32_t dtype;       // gbla_dtype
   int32_t ragged;      // 1 when cu_seqlens describes packed sequences
   float eps;
+  uint32_t flags;      // GBLA_NO_* switches
   int64_t tokens;      // sum of sequence lengths (B*n or T)
 
   // State reduction: the tokens of one (sequence, head) are cut into chunks

@@ -132,7 +132,9 @@ state_stream_kernel(Plan P, const uint16_t* __restrict__ kin, const uint16_t* __
 
   const __amdgpu_buffer_rsrc_t rk = make_rsrc(kin + base_row * D, (uint32_t)(len * 2 * D));
   const __amdgpu_buffer_rsrc_t rv = make_rsrc(vin + base_row * D, (uint32_t)(len * 2 * D));
-  const __amdgpu_buffer_rsrc_t ra = make_rsrc(ain + base_row, (uint32_t)(len * 2));
+  // no logits (uniform gates): an empty range, so every logit reads as 0
+  const __amdgpu_buffer_rsrc_t ra =
+      ain ? make_rsrc(ain + base_row, (uint32_t)(len * 2)) : make_rsrc(kin, 0u);
 
   // Loop-invariant global values first (taps, gate logits), so that the
   // waits for them precede every prefetch.  The key taps carry a factor
@@ -450,7 +452,7 @@ struct RS {
   static constexpr int kLds = 4 * kSlots * kSlotBytes;
 };
 
-template <int D>
+template <int D, bool kNorm>
 __global__ void __launch_bounds__(kThreads, RS<D>::kOcc)
 readout_stream_kernel(Plan P, const uint16_t* __restrict__ qin, const uint16_t* __restrict__ rin,
                       const float* __restrict__ conv_w, const float* __restrict__ gamma,
@@ -470,7 +472,7 @@ readout_stream_kernel(Plan P, const uint16_t* __restrict__ qin, const uint16_t* 
   tile = __builtin_amdgcn_readfirstlane(tile);
   if (tid < D) {
     load_taps4(conv_w, P.heads, h, 0, D, P.W, tid, taps_q[tid]);
-    gam[tid] = gamma[(size_t)h * D + tid];
+    gam[tid] = gamma ? gamma[(size_t)h * D + tid] : 1.0f;
   }
   __syncthreads();
   int64_t len, base_row;
@@ -487,7 +489,9 @@ readout_stream_kernel(Plan P, const uint16_t* __restrict__ qin, const uint16_t* 
   const int n = lane & 15, gq = lane >> 4;
   const size_t sh = (size_t)s * P.heads + h;
   const __amdgpu_buffer_rsrc_t rq = make_rsrc(qin + base_row * D, (uint32_t)(len * C::kRowBytes));
-  const __amdgpu_buffer_rsrc_t rr = make_rsrc(rin + base_row * D, (uint32_t)(len * C::kRowBytes));
+  // kNorm false: out = o (no gated norm) and r is not read
+  const __amdgpu_buffer_rsrc_t rr =
+      kNorm ? make_rsrc(rin + base_row * D, (uint32_t)(len * C::kRowBytes)) : make_rsrc(qin, 0u);
   // stores of tokens at or past r1 fall outside this range and are dropped
   const __amdgpu_buffer_rsrc_t ro = make_rsrc(out + base_row * D, (uint32_t)r1 * (uint32_t)(4 * D));
 
@@ -602,10 +606,20 @@ readout_stream_kernel(Plan P, const uint16_t* __restrict__ qin, const uint16_t* 
           acc[mb][i] *= inv_den;
           ss = fmaf(acc[mb][i], acc[mb][i], ss);
         }
+      const int tok = r0 + grp * C::kGroup + row;
+      if constexpr (!kNorm) {  // out = o
+#pragma unroll
+        for (int qq = 0; qq < NKB; ++qq) {
+          const f32x4_t y0 = acc[2 * qq], y1 = acc[2 * qq + 1];
+          const uint32_t off = (uint32_t)(tok * D + 32 * qq + 8 * gq) * 4u;
+          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, y0), ro, off, 0, 0);
+          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, y1), ro, off + 16, 0, 0);
+        }
+        continue;
+      }
       ss += __shfl_xor(ss, 16);
       ss += __shfl_xor(ss, 32);
       const float scale = __builtin_amdgcn_rsqf(ss * (1.0f / D) + P.eps);
-      const int tok = r0 + grp * C::kGroup + row;
 #pragma unroll
       for (int qq = 0; qq < NKB; ++qq) {
         const u32x4_t rw = rst[jb][qq];
@@ -667,15 +681,19 @@ gbla_status launch_readout_stream(const Plan& p, const void* q, const void* r, c
                                   const float* gamma, const int32_t* cu, const unsigned char* frags,
                                   float* out, hipStream_t st) {
   const dim3 grid(p.runits, p.heads);
-  if (p.d == 128)
-    hipLaunchKernelGGL((readout_stream_kernel<128>), grid, dim3(kThreads), 0, st, p,
-                       (const uint16_t*)q, (const uint16_t*)r, conv_w, gamma, cu, frags, out);
-  else if (p.d == 64)
-    hipLaunchKernelGGL((readout_stream_kernel<64>), grid, dim3(kThreads), 0, st, p,
-                       (const uint16_t*)q, (const uint16_t*)r, conv_w, gamma, cu, frags, out);
-  else
-    hipLaunchKernelGGL((readout_stream_kernel<32>), grid, dim3(kThreads), 0, st, p,
-                       (const uint16_t*)q, (const uint16_t*)r, conv_w, gamma, cu, frags, out);
+  const uint16_t *qq = (const uint16_t*)q, *rr = (const uint16_t*)r;
+#define GBLA_READOUT(DD, NORM)                                                             \
+  hipLaunchKernelGGL((readout_stream_kernel<DD, NORM>), grid, dim3(kThreads), 0, st, p, qq, rr, \
+                     conv_w, gamma, cu, frags, out)
+  const bool norm = gamma != nullptr;  // NULL gamma: the no-gated-norm switch
+  if (p.d == 128) {
+    if (norm) GBLA_READOUT(128, true); else GBLA_READOUT(128, false);
+  } else if (p.d == 64) {
+    if (norm) GBLA_READOUT(64, true); else GBLA_READOUT(64, false);
+  } else {
+    if (norm) GBLA_READOUT(32, true); else GBLA_READOUT(32, false);
+  }
+#undef GBLA_READOUT
   return hipGetLastError() == hipSuccess ? GBLA_OK : GBLA_ERR_HIP;
 }
 

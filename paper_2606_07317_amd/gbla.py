@@ -21,6 +21,11 @@ HEADER_PATH = os.path.join(os.path.dirname(_PKG), "include", "gbla.h")
 
 GBLA_F32 = 0
 GBLA_BF16 = 1
+# Ablation switches (shape.flags); all three together is plain BLA, Eq. (1).
+NO_GATE = 1   # uniform key gates; gate_logits may be None
+NO_CONV = 2   # identity Conv1D; conv_w may be None
+NO_NORM = 4   # out = o; out_gate and norm_w may be None
+BLA = NO_GATE | NO_CONV | NO_NORM
 STATUS_NAMES = {0: "GBLA_OK", 1: "GBLA_ERR_INVALID_ARGUMENT", 2: "GBLA_ERR_UNSUPPORTED",
                 3: "GBLA_ERR_MISALIGNED", 4: "GBLA_ERR_WORKSPACE", 5: "GBLA_ERR_HIP"}
 
@@ -34,7 +39,8 @@ class GblaError(RuntimeError):
 class Shape(ctypes.Structure):
     _fields_ = [("batch", ctypes.c_int32), ("heads", ctypes.c_int32), ("seqlen", ctypes.c_int32),
                 ("head_dim", ctypes.c_int32), ("conv_width", ctypes.c_int32),
-                ("max_seqlen", ctypes.c_int32), ("dtype", ctypes.c_int32), ("eps", ctypes.c_float)]
+                ("max_seqlen", ctypes.c_int32), ("dtype", ctypes.c_int32), ("eps", ctypes.c_float),
+                ("flags", ctypes.c_uint32)]
 
 
 _lib = None
@@ -99,8 +105,9 @@ def _check(t: torch.Tensor, name: str, dtype=None, device=None):
         raise ValueError("%s is on %s, expected %s" % (name, t.device, device))
 
 
-def make_shape(q: torch.Tensor, conv_w: torch.Tensor, eps: float,
-               cu_seqlens: Optional[torch.Tensor], max_seqlen: Optional[int]) -> Shape:
+def make_shape(q: torch.Tensor, conv_w: Optional[torch.Tensor], eps: float,
+               cu_seqlens: Optional[torch.Tensor], max_seqlen: Optional[int],
+               flags: int = 0) -> Shape:
     if cu_seqlens is None:
         if q.dim() != 4:
             raise ValueError("dense q must be [B, H, n, d]")
@@ -112,9 +119,15 @@ def make_shape(q: torch.Tensor, conv_w: torch.Tensor, eps: float,
         H, rows, d = q.shape
         batch = cu_seqlens.numel() - 1
         msl = int(max_seqlen) if max_seqlen is not None else rows
-    if conv_w.dim() != 4 or tuple(conv_w.shape[:3]) != (3, H, d):
-        raise ValueError("conv_w must be [3, H, d, W]")
-    return Shape(batch, H, rows, d, conv_w.shape[3], msl, _dtype_code(q), float(eps))
+    if conv_w is None:
+        if not flags & NO_CONV:
+            raise ValueError("conv_w is required unless flags has NO_CONV")
+        W = 1  # identity conv
+    else:
+        if conv_w.dim() != 4 or tuple(conv_w.shape[:3]) != (3, H, d):
+            raise ValueError("conv_w must be [3, H, d, W]")
+        W = conv_w.shape[3]
+    return Shape(batch, H, rows, d, W, msl, _dtype_code(q), float(eps), int(flags))
 
 
 def _stream(stream) -> int:
@@ -151,7 +164,8 @@ def _check_inputs(q, k, v, a, r, conv_w, norm_w, cu_seqlens):
         _check(a, "gate_logits", q.dtype, dev)
         if a.shape != q.shape[:-1]:
             raise ValueError("gate_logits must have shape %s" % (tuple(q.shape[:-1]),))
-    _check(conv_w, "conv_w", torch.float32, dev)
+    if conv_w is not None:
+        _check(conv_w, "conv_w", torch.float32, dev)
     if norm_w is not None:
         _check(norm_w, "norm_w", torch.float32, dev)
         if norm_w.shape != (q.shape[-3], q.shape[-1]):
@@ -165,10 +179,12 @@ def _ptr(t: Optional[torch.Tensor]):
 
 
 def forward(q, k, v, gate_logits, out_gate, conv_w, norm_w, eps: float = 1e-6,
-            cu_seqlens=None, max_seqlen=None, workspace=None, out=None, stream=None) -> torch.Tensor:
-    """y = GBLA(q, k, v, a, r) on the GPU; see include/gbla.h for the layouts."""
+            cu_seqlens=None, max_seqlen=None, workspace=None, out=None, stream=None,
+            flags: int = 0) -> torch.Tensor:
+    """y = GBLA(q, k, v, a, r) on the GPU (o under NO_NORM); see include/gbla.h
+    for the layouts and the ablation switches in ``flags``."""
     _check_inputs(q, k, v, gate_logits, out_gate, conv_w, norm_w, cu_seqlens)
-    shape = make_shape(q, conv_w, eps, cu_seqlens, max_seqlen)
+    shape = make_shape(q, conv_w, eps, cu_seqlens, max_seqlen, flags)
     if workspace is None:
         workspace = alloc_workspace(shape, q.device)
     if out is None:
@@ -182,11 +198,11 @@ def forward(q, k, v, gate_logits, out_gate, conv_w, norm_w, eps: float = 1e-6,
     return out
 
 
-def conv1d(q, k, v, conv_w, cu_seqlens=None, max_seqlen=None, stream=None
+def conv1d(q, k, v, conv_w, cu_seqlens=None, max_seqlen=None, stream=None, flags: int = 0
            ) -> Tuple[torch.Tensor, torch.Tensor, torch.Tensor]:
     """The Conv1D alone: fp32 q_t, k_t, v_t in the layout of q."""
     _check_inputs(q, k, v, None, None, conv_w, None, cu_seqlens)
-    shape = make_shape(q, conv_w, 0.0, cu_seqlens, max_seqlen)
+    shape = make_shape(q, conv_w, 0.0, cu_seqlens, max_seqlen, flags)
     outs = [torch.empty(q.shape, dtype=torch.float32, device=q.device) for _ in range(3)]
     st = load_library().gbla_conv1d(ctypes.byref(shape), _ptr(q), _ptr(k), _ptr(v), _ptr(conv_w),
                                     _ptr(cu_seqlens), *[_ptr(o) for o in outs], _stream(stream))
@@ -195,10 +211,10 @@ def conv1d(q, k, v, conv_w, cu_seqlens=None, max_seqlen=None, stream=None
 
 
 def state(k, v, gate_logits, conv_w, cu_seqlens=None, max_seqlen=None, workspace=None,
-          stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+          stream=None, flags: int = 0) -> Tuple[torch.Tensor, torch.Tensor]:
     """The normalised global state S [N,H,d,d] and z [N,H,d] (fp32)."""
     _check_inputs(k, k, v, gate_logits, None, conv_w, None, cu_seqlens)
-    shape = make_shape(k, conv_w, 0.0, cu_seqlens, max_seqlen)
+    shape = make_shape(k, conv_w, 0.0, cu_seqlens, max_seqlen, flags)
     if workspace is None:
         workspace = alloc_workspace(shape, k.device)
     N, H, d = shape.batch, shape.heads, shape.head_dim
@@ -212,11 +228,11 @@ def state(k, v, gate_logits, conv_w, cu_seqlens=None, max_seqlen=None, workspace
 
 
 def readout(q, out_gate, conv_w, norm_w, workspace, eps: float = 1e-6, cu_seqlens=None,
-            max_seqlen=None, out=None, stream=None) -> torch.Tensor:
+            max_seqlen=None, out=None, stream=None, flags: int = 0) -> torch.Tensor:
     """Readout + gated RMSNorm from the state a preceding state() call left in
     ``workspace``."""
     _check_inputs(q, None, None, None, out_gate, conv_w, norm_w, cu_seqlens)
-    shape = make_shape(q, conv_w, eps, cu_seqlens, max_seqlen)
+    shape = make_shape(q, conv_w, eps, cu_seqlens, max_seqlen, flags)
     if out is None:
         out = torch.empty(q.shape, dtype=torch.float32, device=q.device)
     st = load_library().gbla_readout(ctypes.byref(shape), _ptr(q), _ptr(out_gate), _ptr(conv_w),

@@ -101,3 +101,28 @@ def test_other_entry_points_reject_before_launch(lib):
     assert lib.gbla_readout(ctypes.byref(s), None, P, P, P, None, P, 1 << 40, P, None) == 1
     assert lib.gbla_readout(ctypes.byref(s), P, P, P, P, None, None, 1 << 40, P, None) == 4
     assert lib.gbla_readout(ctypes.byref(s), P, P, P, P, None, P, 0, P, None) == 4
+
+
+def test_ablation_switches_validation(lib):
+    """Inputs removed by a switch may be NULL (or anything) and are not
+    checked; unknown flag bits are rejected.  Each call still fails on the
+    missing workspace, which is checked after the inputs, so nothing launches."""
+    assert lib.gbla_workspace_bytes(ctypes.byref(shape(flags=8))) == 0
+    assert _forward(lib, shape(flags=8)) == 1
+    assert _forward(lib, shape(), a=None, ws=None) == 1
+    assert _forward(lib, shape(flags=gbla.NO_GATE), a=None, ws=None) == 4
+    assert _forward(lib, shape(), w=None, ws=None) == 1
+    assert _forward(lib, shape(flags=gbla.NO_CONV), w=None, ws=None) == 4
+    assert _forward(lib, shape(flags=gbla.NO_CONV), w=ALIGNED + 4, ws=None) == 4
+    assert _forward(lib, shape(), r=None, g=None, ws=None) == 1
+    assert _forward(lib, shape(flags=gbla.NO_NORM), r=None, g=None, ws=None) == 4
+    assert _forward(lib, shape(flags=gbla.BLA), a=None, r=None, w=None, g=None, ws=None) == 4
+    # the switches do not relax the inputs they leave in use
+    assert _forward(lib, shape(flags=gbla.BLA), q=None, ws=None) == 1
+    P = ALIGNED
+    assert lib.gbla_state(ctypes.byref(shape(flags=gbla.NO_GATE)), P, P, None, P, None,
+                          None, 0, P, P, None) == 4
+    assert lib.gbla_readout(ctypes.byref(shape(flags=gbla.NO_NORM)), P, None, P, None, None,
+                            None, 0, P, None) == 4
+    assert lib.gbla_conv1d(ctypes.byref(shape(flags=gbla.NO_CONV, head_dim=16)), P, P, P, None,
+                           None, P, P, P, None) == 2

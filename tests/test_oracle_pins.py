@@ -338,6 +338,27 @@ def test_reduces_to_bla_eq1(orc):
             np.testing.assert_allclose(o[s, h], num / den[:, None], rtol=1e-12)
 
 
+def test_ablation_switches_reach_bla_eq1(orc):
+    """The oracle's ablation switches (the paper's ablation table): with key
+    gating, Conv1D and the gated norm all switched off, forward_inputs returns
+    Eq. (1) evaluated in numpy's matrix form."""
+    inp = gin.make_inputs(gin.WORKLOADS["b8_n2048_d64"].with_(batch=2, heads=2, seqlen=37,
+                                                              head_dim=32, seed=78))
+    o = orc.forward_inputs(inp, want=("y",), gate=False, conv=False, norm=False)["y"]
+    dt = inp.workload.dtype
+    q, k, v = (gin.to_f64(x, dt) for x in (inp.q, inp.k, inp.v))
+    for s in range(2):
+        for h in range(2):
+            fq, fk = phi_np(q[s, h]), phi_np(k[s, h])
+            num = fq @ (fk.T @ v[s, h])
+            den = fq @ fk.sum(axis=0)
+            np.testing.assert_allclose(o[s, h], num / den[:, None], rtol=1e-12)
+    # each switch alone changes the result (it is wired to something)
+    y = orc.forward_inputs(inp, want=("y",))["y"]
+    for kw in (dict(gate=False), dict(conv=False), dict(norm=False)):
+        assert np.abs(orc.forward_inputs(inp, want=("y",), **kw)["y"] - y).max() > 1e-6, kw
+
+
 # --------------------------------------------------------------------------
 # The paper's placement: Conv1D on X, projections after (Section 2.1 item 1).
 # With channel-shared taps the conv commutes with the projections, so the

@@ -160,6 +160,63 @@ def test_forward_parity_ragged64_d128(G, dev, orc):
     close(y, ref, TOL[inp.workload.dtype], "y ragged64_d128")
 
 
+# Ablation switches (the paper's ablation table): each alone and all three
+# (BLA, Eq. (1)), on the bf16 and fp32 paths, d = 32 / 64 / 128, dense and ragged.
+SWITCH_CASES = ["bf16_d64_n1000", "f32_d64_n1000", "ragged_d128_mixed", "bf16_d32_n3001_W2"]
+
+
+def _case(name):
+    if name in SMALL_CASES:
+        return SMALL_CASES[name], None
+    return RAGGED_CASES[name]
+
+
+def _switch_flags(G, sw):
+    return {"no_gate": G.NO_GATE, "no_conv": G.NO_CONV, "no_norm": G.NO_NORM, "bla": G.BLA}[sw]
+
+
+@pytest.mark.parametrize("sw", ["no_gate", "no_conv", "no_norm", "bla"])
+@pytest.mark.parametrize("name", SWITCH_CASES)
+def test_forward_switch_parity(G, dev, orc, name, sw):
+    say("forward switch", sw, name)
+    w, lens = _case(name)
+    flags = _switch_flags(G, sw)
+    inp = inputs.make_inputs(w, lengths=lens)
+    t = inputs.device_tensors(inp, dev)
+    # inputs a switch removes are passed as None: the library must not read them
+    a = None if flags & G.NO_GATE else t["a"]
+    cw = None if flags & G.NO_CONV else t["conv_w"]
+    r = None if flags & G.NO_NORM else t["r"]
+    gm = None if flags & G.NO_NORM else t["gamma"]
+    y = G.forward(t["q"], t["k"], t["v"], a, r, cw, gm, eps=inp.eps, cu_seqlens=t["cu_seqlens"],
+                  max_seqlen=t["max_seqlen"], flags=flags)
+    torch.cuda.synchronize()
+    ref = orc.forward_inputs(inp, want=("y",), gate=not flags & G.NO_GATE,
+                             conv=not flags & G.NO_CONV, norm=not flags & G.NO_NORM)["y"]
+    close(y.cpu().numpy(), ref, TOL[w.dtype], "y " + sw)
+
+
+@pytest.mark.parametrize("name", ["bf16_d64_n1000", "ragged_d128_mixed"])
+def test_state_and_conv_switches(G, dev, orc, name):
+    say("state/conv switches", name)
+    w, lens = _case(name)
+    inp = inputs.make_inputs(w, lengths=lens)
+    t = inputs.device_tensors(inp, dev)
+    # uniform gates: S and z carry g_j = 1/n
+    S, z = G.state(t["k"], t["v"], None, t["conv_w"], cu_seqlens=t["cu_seqlens"],
+                   max_seqlen=t["max_seqlen"], flags=G.NO_GATE)
+    torch.cuda.synchronize()
+    ref = orc.forward_inputs(inp, want=("S", "z"), gate=False)
+    close(S.cpu().numpy(), ref["S"], TOL[w.dtype], "S no_gate")
+    close(z.cpu().numpy(), ref["z"], TOL[w.dtype], "z no_gate")
+    # identity conv returns the inputs exactly
+    qt, kt, vt = G.conv1d(t["q"], t["k"], t["v"], None, cu_seqlens=t["cu_seqlens"],
+                          max_seqlen=t["max_seqlen"], flags=G.NO_CONV)
+    torch.cuda.synchronize()
+    for got, x in ((qt, t["q"]), (kt, t["k"]), (vt, t["v"])):
+        assert torch.equal(got, x.float()), "identity conv must return its input"
+
+
 def test_state_then_readout_equals_forward(G, dev):
     say("state+readout == forward")
     inp = inputs.make_inputs(SMALL_CASES["bf16_d64_n1000"])
