@@ -1,0 +1,175 @@
+"""Plain fp64 oracle of the GBLA backward pass (the chain rule through the
+forward pass of Section 2 and Section 2.1 of the paper).
+
+TEST INFRASTRUCTURE ONLY: the tests use it; the product path never imports
+it, and it shares no code with the HIP library.
+
+The paper gives the forward pass only.  This module differentiates it step
+by step, in reverse order, for one sequence s and one head h (tokens i, j;
+channels c, e), with every quantity in fp64 and every sum taken by numpy in
+index order.  Forward quantities are recomputed first:
+
+    xt = Conv1D(x) for x in q, k, v        (Section 2.1, "Conv1D")
+    Qh = phi(qt),  P = phi(kt)             (phi = elu + 1, Section 2)
+    g  = softmax(a)                        (Section 2.1, "Key gating")
+    S  = sum_j g_j P_j vt_j^T,  z = sum_j g_j P_j
+    num_i = Qh_i^T S,  den_i = Qh_i^T z,  o_i = num_i / den_i
+    rs_i = (mean_e o_ie^2 + eps)^(-1/2),  oh_i = rs_i o_i
+    y_i = oh_i * gamma * silu(r_i)        (Section 2.1, "RMSNorm with gating")
+
+Then, given dy = dL/dy:
+
+    1. gated norm:  doh = dy gamma silu(r);  dgamma += sum_i dy oh silu(r);
+                    dr = dy oh gamma silu'(r),
+                    silu'(x) = sigma(x) (1 + x (1 - sigma(x)))
+    2. RMSNorm:     do_i = rs_i doh_i - rs_i^3 (1/d) (doh_i . o_i) o_i
+    3. division:    dnum_i = do_i / den_i,  dden_i = -(do_i . o_i) / den_i
+    4. readout:     dQh_i = S dnum_i + z dden_i
+                    dS = sum_i Qh_i dnum_i^T,  dz = sum_i Qh_i dden_i
+    5. state:       t_j = dS vt_j + dz
+                    dP_j = g_j t_j,  dvt_j = g_j dS^T P_j,  dg_j = P_j . t_j
+    6. softmax:     da_j = g_j (dg_j - sum_l g_l dg_l)
+    7. feature map: dqt = dQh phi'(qt),  dkt = dP phi'(kt),
+                    phi'(u) = 1 for u > 0, exp(u) otherwise
+    8. Conv1D:      dx_m = sum_t w_t dxt_{m+W-1-t} (tokens past the end of the
+                    sequence contribute nothing), and
+                    dw_t += sum_i dxt_i x_{i-W+1+t} (x = 0 before the start).
+
+dgamma and the tap gradients are summed over every sequence of the batch.
+"""
+from __future__ import annotations
+
+from typing import Optional
+
+import numpy as np
+
+
+def _widen(x, dtype: str) -> np.ndarray:
+    """Exact fp64 value of stored activations (bf16 as uint16 bit patterns)."""
+    x = np.asarray(x)
+    if dtype == "bf16":
+        return (x.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    return x.astype(np.float64)
+
+
+def _phi(u):
+    return np.where(u > 0, u + 1.0, np.exp(np.minimum(u, 0.0)))
+
+
+def _dphi(u):
+    return np.where(u > 0, 1.0, np.exp(np.minimum(u, 0.0)))
+
+
+def _conv(x, w):
+    """Causal depthwise conv of one [L, d] slice, taps [d, W] (tap W-1 on the
+    current token), zero before the start."""
+    L, d = x.shape
+    W = w.shape[1]
+    out = np.zeros_like(x)
+    for t in range(W):
+        sh = W - 1 - t                       # x_{i - sh}
+        if sh < L:
+            out[sh:] += w[:, t] * x[:L - sh]
+    return out
+
+
+def _conv_backward(x, dxt, w):
+    """Gradients of _conv: (dx [L, d], dw [d, W])."""
+    L, d = x.shape
+    W = w.shape[1]
+    dx = np.zeros_like(x)
+    dw = np.zeros((d, W))
+    for t in range(W):
+        sh = W - 1 - t
+        if sh < L:
+            dx[:L - sh] += w[:, t] * dxt[sh:]
+            dw[:, t] += np.sum(dxt[sh:] * x[:L - sh], axis=0)
+    return dx, dw
+
+
+def _one(q, k, v, a, r, cw, gamma, dy, eps):
+    """Backward of one (sequence, head): returns the input gradients and this
+    slice's contributions to dconv_w [3, d, W] and dgamma [d]."""
+    L, d = q.shape
+    if L == 0:
+        z0 = np.zeros((0, d))
+        return z0, z0, z0, np.zeros(0), z0, np.zeros((3, d, cw.shape[-1])), np.zeros(d)
+    qt, kt, vt = _conv(q, cw[0]), _conv(k, cw[1]), _conv(v, cw[2])
+    Qh, P = _phi(qt), _phi(kt)
+    e = np.exp(a - a.max())
+    g = e / e.sum()
+    S = (g[:, None] * P).T @ vt
+    z = (g[:, None] * P).sum(axis=0)
+    num = Qh @ S
+    den = Qh @ z
+    o = num / den[:, None]
+    rs = 1.0 / np.sqrt(np.mean(o * o, axis=1) + eps)
+    oh = o * rs[:, None]
+    sig = 1.0 / (1.0 + np.exp(-r))
+    silu = r * sig
+    # 1. gated norm
+    doh = dy * gamma * silu
+    dgamma = np.sum(dy * oh * silu, axis=0)
+    dr = dy * oh * gamma * sig * (1.0 + r * (1.0 - sig))
+    # 2. RMSNorm
+    do = rs[:, None] * doh - (rs ** 3 / d * np.sum(doh * o, axis=1))[:, None] * o
+    # 3. division
+    dnum = do / den[:, None]
+    dden = -np.sum(do * o, axis=1) / den
+    # 4. readout
+    dQh = dnum @ S.T + dden[:, None] * z[None, :]
+    dS = Qh.T @ dnum
+    dz = Qh.T @ dden
+    # 5. state
+    t = vt @ dS.T + dz[None, :]
+    dP = g[:, None] * t
+    dvt = g[:, None] * (P @ dS)
+    dg = np.sum(P * t, axis=1)
+    # 6. softmax
+    da = g * (dg - np.sum(g * dg))
+    # 7. feature map
+    dqt = dQh * _dphi(qt)
+    dkt = dP * _dphi(kt)
+    # 8. Conv1D
+    dq, dwq = _conv_backward(q, dqt, cw[0])
+    dk, dwk = _conv_backward(k, dkt, cw[1])
+    dv, dwv = _conv_backward(v, dvt, cw[2])
+    return dq, dk, dv, da, dr, np.stack([dwq, dwk, dwv]), dgamma
+
+
+def backward(q, k, v, a, r, conv_w, gamma, dy, *, nseq: int, heads: int, rows: int, d: int,
+             W: int, dtype: str, eps: float, cu_seqlens: Optional[np.ndarray] = None) -> dict:
+    """Gradients of sum(y * dy) with respect to every input of the forward
+    pass.  Layouts as in the forward oracle: dense [nseq, H, rows, d] or
+    ragged [H, T, d] with ``cu_seqlens``; logits without the trailing d.
+    Returns fp64 dq, dk, dv, da, dr (input layouts), dconv_w [3, H, d, W] and
+    dgamma [H, d]."""
+    acts = [_widen(x, dtype) for x in (q, k, v, a, r)]
+    dyv = np.asarray(dy, dtype=np.float64)
+    cw = np.asarray(conv_w, dtype=np.float64).reshape(3, heads, d, W)
+    gm = np.asarray(gamma, dtype=np.float64).reshape(heads, d)
+    if cu_seqlens is None:
+        shp = (nseq, heads, rows, d)
+        acts = [x.reshape(shp if i != 3 else shp[:-1]) for i, x in enumerate(acts)]
+        dyv = dyv.reshape(shp)
+    else:
+        shp = (heads, rows, d)
+        acts = [x.reshape(shp if i != 3 else shp[:-1]) for i, x in enumerate(acts)]
+        dyv = dyv.reshape(shp)
+    qa, ka, va, aa, ra = acts
+    out = {n: np.zeros(qa.shape) for n in ("dq", "dk", "dv", "dr")}
+    out["da"] = np.zeros(aa.shape)
+    out["dconv_w"] = np.zeros((3, heads, d, W))
+    out["dgamma"] = np.zeros((heads, d))
+    for s in range(nseq):
+        for h in range(heads):
+            if cu_seqlens is None:
+                sl = (s, h)
+            else:
+                sl = (h, slice(int(cu_seqlens[s]), int(cu_seqlens[s + 1])))
+            res = _one(qa[sl], ka[sl], va[sl], aa[sl], ra[sl], cw[:, h], gm[h], dyv[sl], eps)
+            for name, val in zip(("dq", "dk", "dv", "da", "dr"), res[:5]):
+                out[name][sl] = val
+            out["dconv_w"][:, h] += res[5]
+            out["dgamma"][h] += res[6]
+    return out

@@ -1,0 +1,104 @@
+"""Pins of the fp64 backward oracle (oracle/gbla_backward.py).
+
+Every gradient is checked against central finite differences of the C forward
+oracle (a separate implementation of the forward pass) on the scalar
+L = sum(y * dy): a dropped term, a wrong sign or a transposed operand in any
+step of the chain rule fails here.  No GPU is needed.
+"""
+import numpy as np
+import pytest
+
+from oracle import gbla_backward
+
+
+def problem(seed, nseq=2, H=2, n=9, d=5, W=4, ragged=None):
+    rng = np.random.default_rng(seed)
+    if ragged is None:
+        shp = (nseq, H, n, d)
+        cu = None
+        rows = n
+    else:
+        cu = np.concatenate([[0], np.cumsum(ragged)]).astype(np.int32)
+        nseq, rows = len(ragged), int(cu[-1])
+        shp = (H, rows, d)
+    p = {x: rng.standard_normal(shp) for x in ("q", "k", "v", "r")}
+    p["a"] = rng.standard_normal(shp[:-1])
+    p["conv_w"] = 0.5 * rng.standard_normal((3, H, d, W))
+    p["gamma"] = 1.0 + 0.1 * rng.standard_normal((H, d))
+    dy = rng.standard_normal(shp)
+    meta = dict(nseq=nseq, heads=H, rows=rows, d=d, W=W, dtype="f64", eps=1e-3, cu_seqlens=cu)
+    return p, dy, meta
+
+
+def loss(orc, p, dy, meta):
+    y = orc.forward(p["q"], p["k"], p["v"], p["a"], p["r"], p["conv_w"], p["gamma"],
+                    want=("y",), **meta)["y"]
+    return float(np.sum(y * dy))
+
+
+GRAD_OF = {"q": "dq", "k": "dk", "v": "dv", "a": "da", "r": "dr", "conv_w": "dconv_w",
+           "gamma": "dgamma"}
+
+
+def check_fd(orc, p, dy, meta, samples=6, seed=0, h=1e-5):
+    g = gbla_backward.backward(p["q"], p["k"], p["v"], p["a"], p["r"], p["conv_w"], p["gamma"],
+                               dy, **meta)
+    rng = np.random.default_rng(seed)
+    for name, gname in GRAD_OF.items():
+        x = p[name]
+        assert g[gname].shape == x.shape, (gname, g[gname].shape, x.shape)
+        for flat in rng.choice(x.size, size=min(samples, x.size), replace=False):
+            idx = np.unravel_index(flat, x.shape)
+            xp, xm = x.copy(), x.copy()
+            xp[idx] += h
+            xm[idx] -= h
+            fd = (loss(orc, dict(p, **{name: xp}), dy, meta) -
+                  loss(orc, dict(p, **{name: xm}), dy, meta)) / (2 * h)
+            got = g[gname][idx]
+            assert abs(got - fd) <= 1e-6 + 1e-5 * abs(fd), (gname, idx, got, fd)
+
+
+@pytest.mark.parametrize("W", [1, 2, 4])
+def test_backward_matches_finite_differences_dense(orc, W):
+    p, dy, meta = problem(10 + W, W=W)
+    check_fd(orc, p, dy, meta, seed=W)
+
+
+def test_backward_matches_finite_differences_ragged(orc):
+    # an empty sequence, a one-token sequence and sequences shorter than W
+    p, dy, meta = problem(21, H=2, d=4, W=4, ragged=[5, 0, 1, 3, 8])
+    check_fd(orc, p, dy, meta, samples=8, seed=3)
+
+
+def test_backward_of_linear_pieces(orc):
+    """Closed forms: L is linear in gamma, so dgamma is exactly
+    sum_i dy oh silu(r) from the forward oracle's oh; and the softmax gradient
+    sums to zero over each sequence (logits are shift invariant)."""
+    p, dy, meta = problem(31)
+    g = gbla_backward.backward(p["q"], p["k"], p["v"], p["a"], p["r"], p["conv_w"], p["gamma"],
+                               dy, **meta)
+    oh = orc.forward(p["q"], p["k"], p["v"], p["a"], p["r"], p["conv_w"], p["gamma"],
+                     want=("oh",), **meta)["oh"]
+    silu = p["r"] / (1.0 + np.exp(-p["r"]))
+    np.testing.assert_allclose(g["dgamma"], np.einsum("shie->he", dy * oh * silu), rtol=1e-12)
+    np.testing.assert_allclose(g["da"].sum(axis=-1), 0.0, atol=1e-12)
+
+
+def test_gate_gradient_has_no_centering_term(orc):
+    """o is invariant to scaling all gates of a sequence (the normaliser cancels
+    between numerator and denominator), so by Euler's theorem
+    sum_j g_j dL/dg_j = 0 and the softmax Jacobian's centering term vanishes:
+    da_j = g_j dL/dg_j.  The oracle with that term removed must agree with the
+    full one to rounding on random data."""
+    import types
+    src = open(gbla_backward.__file__).read()
+    old = "da = g * (dg - np.sum(g * dg))"
+    assert src.count(old) == 1
+    mod = types.ModuleType("gbla_backward_no_center")
+    exec(compile(src.replace(old, "da = g * dg"), gbla_backward.__file__, "exec"), mod.__dict__)
+    for seed in (51, 52):
+        p, dy, meta = problem(seed, nseq=3)
+        args = (p["q"], p["k"], p["v"], p["a"], p["r"], p["conv_w"], p["gamma"], dy)
+        full = gbla_backward.backward(*args, **meta)["da"]
+        nocenter = mod.backward(*args, **meta)["da"]
+        np.testing.assert_allclose(nocenter, full, rtol=1e-9, atol=1e-14)
