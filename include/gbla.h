@@ -152,6 +152,41 @@ gbla_status gbla_readout(const gbla_shape* shape, const void* q, const void* out
                          const int32_t* cu_seqlens, void* workspace,
                          size_t workspace_bytes, float* out, void* stream);
 
+/*
+ * Bytes of device scratch that gbla_backward needs for this shape (dense or
+ * ragged); 0 for an invalid shape.  About 12 * tokens * H * d bytes (fp32
+ * gradients of the convolved q, k, v) plus per-chunk partials.
+ */
+size_t gbla_backward_workspace_bytes(const gbla_shape* shape);
+
+/*
+ * Gradients of L = sum(out * dy) with respect to every input of gbla_forward:
+ * the chain rule through the forward pass of Section 2.1 (Conv1D, key gating,
+ * the global state, the readout, the gated RMSNorm), the forward quantities
+ * recomputed from the inputs.  The paper defines the forward only; the
+ * backward is its exact derivative (the gates need no softmax centering
+ * term: the output does not change when every gate of a sequence is scaled
+ * by one factor).
+ *   q ... cu_seqlens  the inputs of the gbla_forward call, same layouts
+ *   dy               [B,H,n,d] or [H,T,d] fp32, dL/dout
+ *   workspace        >= gbla_backward_workspace_bytes(shape) bytes
+ *   dq, dk, dv       [B,H,n,d] or [H,T,d] fp32
+ *   d_gate_logits    [B,H,n]   or [H,T]   fp32
+ *   d_out_gate       [B,H,n,d] or [H,T,d] fp32
+ *   d_conv_w         [3,H,d,W] fp32, summed over the batch
+ *   d_norm_w         [H,d]     fp32, summed over the batch
+ * Every output is overwritten (not accumulated).  Reductions run in an order
+ * fixed by the shape: repeated calls give the same bits.  Only the full layer
+ * (shape->flags == 0) is built: other flags return GBLA_ERR_UNSUPPORTED.
+ */
+gbla_status gbla_backward(const gbla_shape* shape, const void* q, const void* k,
+                          const void* v, const void* gate_logits, const void* out_gate,
+                          const float* conv_w, const float* norm_w,
+                          const int32_t* cu_seqlens, const float* dy, void* workspace,
+                          size_t workspace_bytes, float* dq, float* dk, float* dv,
+                          float* d_gate_logits, float* d_out_gate, float* d_conv_w,
+                          float* d_norm_w, void* stream);
+
 /* A static, human-readable name of a status code (never NULL). */
 const char* gbla_status_string(gbla_status status);
 

@@ -173,3 +173,14 @@ def backward(q, k, v, a, r, conv_w, gamma, dy, *, nseq: int, heads: int, rows: i
             out["dconv_w"][:, h] += res[5]
             out["dgamma"][h] += res[6]
     return out
+
+
+def backward_inputs(inp, dy) -> dict:
+    """``backward`` on a ``paper_2606_07317_amd.inputs.Inputs`` batch and its
+    cotangent ``dy``."""
+    w = inp.workload
+    ragged = inp.cu_seqlens is not None
+    return backward(inp.q, inp.k, inp.v, inp.a, inp.r, inp.conv_w, inp.gamma, dy,
+                    nseq=inp.nseq, heads=w.heads, rows=inp.rows if ragged else w.seqlen,
+                    d=w.head_dim, W=w.conv_width, dtype=w.dtype, eps=inp.eps,
+                    cu_seqlens=inp.cu_seqlens)

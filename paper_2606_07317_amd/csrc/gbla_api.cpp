@@ -94,6 +94,28 @@ gbla_status make_plan(const gbla_shape* s, bool ragged, Plan* p) {
   return GBLA_OK;
 }
 
+BwdLayout make_bwd_layout(const Plan& p) {
+  BwdLayout L{};
+  const size_t pairs = (size_t)p.nseq * p.heads, d = p.d, f = sizeof(float);
+  const size_t unit_recs = (size_t)p.units * p.heads;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off = align_up(off + bytes, 256);
+    return at;
+  };
+  L.off_S = take(pairs * d * d * f);
+  L.off_z = take(pairs * d * f);
+  L.off_mz = take(pairs * 2 * f);
+  L.off_dsp = take(unit_recs * p.rec_floats * f);
+  L.off_dS = take(pairs * (d * d + d) * f);
+  L.off_dgp = take(unit_recs * d * f);
+  L.off_dxt = take(3 * (size_t)p.tokens * p.heads * d * f);
+  L.off_dcp = take(unit_recs * 3 * d * 4 * f);
+  L.total_bytes = off;
+  return L;
+}
+
 }  // namespace gbla
 
 using gbla::Plan;
@@ -176,7 +198,7 @@ gbla_status gbla_forward(const gbla_shape* shape, const void* q, const void* k, 
   GBLA_TRY(check_ws(p, workspace, workspace_bytes));
   hipStream_t st = static_cast<hipStream_t>(stream);
   GBLA_TRY(gbla::launch_state(p, k, v, gate_logits, conv_w, cu_seqlens, workspace, nullptr,
-                              nullptr, st));
+                              nullptr, nullptr, st));
   return gbla::launch_readout(p, q, out_gate, conv_w, norm_w, cu_seqlens, workspace, out, st);
 }
 
@@ -204,7 +226,7 @@ gbla_status gbla_state(const gbla_shape* shape, const void* k, const void* v,
   if (!(p.flags & GBLA_NO_CONV)) GBLA_TRY(check_used({conv_w}));
   if (!(p.flags & GBLA_NO_GATE)) GBLA_TRY(check_logits(p, gate_logits));
   GBLA_TRY(check_ws(p, workspace, workspace_bytes));
-  return gbla::launch_state(p, k, v, gate_logits, conv_w, cu_seqlens, workspace, S, z,
+  return gbla::launch_state(p, k, v, gate_logits, conv_w, cu_seqlens, workspace, S, z, nullptr,
                             static_cast<hipStream_t>(stream));
 }
 
@@ -222,6 +244,38 @@ gbla_status gbla_readout(const gbla_shape* shape, const void* q, const void* out
   GBLA_TRY(check_ws(p, workspace, workspace_bytes));
   return gbla::launch_readout(p, q, out_gate, conv_w, norm_w, cu_seqlens, workspace, out,
                               static_cast<hipStream_t>(stream));
+}
+
+size_t gbla_backward_workspace_bytes(const gbla_shape* shape) {
+  Plan dense, ragged;
+  if (gbla::make_plan(shape, false, &dense) != GBLA_OK) return 0;
+  if (gbla::make_plan(shape, true, &ragged) != GBLA_OK) return 0;
+  const size_t a = gbla::make_bwd_layout(dense).total_bytes;
+  const size_t b = gbla::make_bwd_layout(ragged).total_bytes;
+  return a > b ? a : b;
+}
+
+gbla_status gbla_backward(const gbla_shape* shape, const void* q, const void* k, const void* v,
+                          const void* gate_logits, const void* out_gate, const float* conv_w,
+                          const float* norm_w, const int32_t* cu_seqlens, const float* dy,
+                          void* workspace, size_t workspace_bytes, float* dq, float* dk,
+                          float* dv, float* d_gate_logits, float* d_out_gate, float* d_conv_w,
+                          float* d_norm_w, void* stream) {
+  Plan p;
+  GBLA_TRY(gbla::make_plan(shape, cu_seqlens != nullptr, &p));
+  if (p.flags != 0) return GBLA_ERR_UNSUPPORTED;
+  GBLA_TRY(check_acts(p, {q, k, v, out_gate, dy, dq, dk, dv, d_out_gate}));
+  GBLA_TRY(check_used({conv_w, norm_w, d_conv_w, d_norm_w}));
+  GBLA_TRY(check_logits(p, gate_logits));
+  if (!d_gate_logits) return GBLA_ERR_INVALID_ARGUMENT;
+  if (!gbla::aligned(d_gate_logits, sizeof(float))) return GBLA_ERR_MISALIGNED;
+  const gbla::BwdLayout L = gbla::make_bwd_layout(p);
+  if (!workspace) return GBLA_ERR_WORKSPACE;
+  if (!gbla::aligned(workspace, 256)) return GBLA_ERR_MISALIGNED;
+  if (workspace_bytes < L.total_bytes) return GBLA_ERR_WORKSPACE;
+  return gbla::launch_backward(p, L, q, k, v, gate_logits, out_gate, conv_w, norm_w, cu_seqlens,
+                               dy, workspace, dq, dk, dv, d_gate_logits, d_out_gate, d_conv_w,
+                               d_norm_w, static_cast<hipStream_t>(stream));
 }
 
 const char* gbla_status_string(gbla_status status) {

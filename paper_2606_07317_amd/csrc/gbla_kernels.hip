@@ -440,7 +440,8 @@ constexpr int kCombineStage = 1024;  // chunk weights staged in LDS per round
 template <typename T, int D, int E>
 __global__ void __launch_bounds__(kThreads)
 combine_kernel(Plan P, const int32_t* __restrict__ cu, const float* __restrict__ partials,
-               float* __restrict__ S_out, float* __restrict__ z_out, unsigned char* __restrict__ frags) {
+               float* __restrict__ S_out, float* __restrict__ z_out, unsigned char* __restrict__ frags,
+               float* __restrict__ mz_out) {
   constexpr int kElems = D * D + D;
   __shared__ float red[kThreads / 64];
   __shared__ float wst[kCombineStage];
@@ -491,6 +492,11 @@ combine_kernel(Plan P, const int32_t* __restrict__ cu, const float* __restrict__
 #pragma unroll
   for (int w = 0; w < kThreads / 64; ++w) Z += red[w];
   const float invZ = Z > 0.0f ? 1.0f / Z : 0.0f;
+  // (M, Z) of the sequence's softmax, for the backward pass
+  if (mz_out && blockIdx.y == 0 && tid == 0) {
+    mz_out[2 * (size_t)sh_idx] = M;
+    mz_out[2 * (size_t)sh_idx + 1] = Z;
+  }
 
   int xe[E];
   float v[E];
@@ -523,7 +529,7 @@ combine_kernel(Plan P, const int32_t* __restrict__ cu, const float* __restrict__
   }
 
   const size_t sh = (size_t)s * P.heads + h;
-  unsigned char* fr = frags + sh * P.frag_bytes;
+  unsigned char* fr = frags ? frags + sh * P.frag_bytes : nullptr;
 #pragma unroll
   for (int e = 0; e < E; ++e) {
     const int x = (blockIdx.y * E + e) * kThreads + tid;
@@ -534,12 +540,13 @@ combine_kernel(Plan P, const int32_t* __restrict__ cu, const float* __restrict__
       if (S_out) S_out[sh * D * D + x] = val;
       const int kb = c / 32, gq = (c % 32) / 8, j = c % 8;
       const int mb = 2 * (ee / 32) + (ee % 8) / 4, m = 4 * ((ee % 32) / 8) + ee % 4;
-      frag_put<T, D>(fr, mb, kb, 16 * gq + m, j, val);
+      if (fr) frag_put<T, D>(fr, mb, kb, 16 * gq + m, j, val);
     } else {
       const int c = x - D * D;
       if (z_out) z_out[sh * D + c] = val;
       const int kb = c / 32, gq = (c % 32) / 8, j = c % 8;
-      for (int m = 0; m < 16; ++m) frag_put<T, D>(fr, D / 16, kb, 16 * gq + m, j, val);
+      if (fr)
+        for (int m = 0; m < 16; ++m) frag_put<T, D>(fr, D / 16, kb, 16 * gq + m, j, val);
     }
   }
 }
@@ -818,11 +825,30 @@ struct ConvRun {
   }
 };
 
+// One element per thread while the grid stays small; four once there are
+// many (sequence, head) pairs.  The result does not depend on the choice.
+template <typename T, int D>
+gbla_status run_combine(const Plan& p, const int32_t* cu, const float* partials, float* S,
+                        float* z, unsigned char* frags, float* mz, hipStream_t st) {
+  constexpr int kElems = D * D + D;
+  const int64_t pairs = (int64_t)p.nseq * p.heads;
+  const int slices1 = (kElems + kThreads - 1) / kThreads;
+  if (pairs * slices1 <= 4096) {
+    hipLaunchKernelGGL((combine_kernel<T, D, 1>), dim3(pairs, slices1), dim3(kThreads), 0, st, p,
+                       cu, partials, S, z, frags, mz);
+  } else {
+    const int slices4 = (kElems + 4 * kThreads - 1) / (4 * kThreads);
+    hipLaunchKernelGGL((combine_kernel<T, D, 4>), dim3(pairs, slices4), dim3(kThreads), 0, st, p,
+                       cu, partials, S, z, frags, mz);
+  }
+  return last_launch_status();
+}
+
 template <typename T, int D>
 struct StateRun {
   static gbla_status run(const Plan& p, const void* k, const void* v, const void* a,
                          const float* w, const int32_t* cu, void* ws, float* S, float* z,
-                         hipStream_t st) {
+                         float* mz, hipStream_t st) {
     unsigned char* base = static_cast<unsigned char*>(ws);
     float* partials = reinterpret_cast<float*>(base + p.off_partials);
     gbla_status e;
@@ -834,20 +860,15 @@ struct StateRun {
       e = last_launch_status();
     }
     if (e != GBLA_OK) return e;
-    // One element per thread while the grid stays small; four once there are
-    // many (sequence, head) pairs.  The result does not depend on the choice.
-    constexpr int kElems = D * D + D;
-    const int64_t pairs = (int64_t)p.nseq * p.heads;
-    const int slices1 = (kElems + kThreads - 1) / kThreads;
-    if (pairs * slices1 <= 4096) {
-      hipLaunchKernelGGL((combine_kernel<T, D, 1>), dim3(pairs, slices1), dim3(kThreads), 0,
-                         st, p, cu, (const float*)partials, S, z, base + p.off_frags);
-    } else {
-      const int slices4 = (kElems + 4 * kThreads - 1) / (4 * kThreads);
-      hipLaunchKernelGGL((combine_kernel<T, D, 4>), dim3(pairs, slices4), dim3(kThreads), 0,
-                         st, p, cu, (const float*)partials, S, z, base + p.off_frags);
-    }
-    return last_launch_status();
+    return run_combine<T, D>(p, cu, partials, S, z, base + p.off_frags, mz, st);
+  }
+};
+
+template <typename T, int D>
+struct CombineF32Run {
+  static gbla_status run(const Plan& p, const int32_t* cu, const float* partials, float* S,
+                         float* z, float* mz, hipStream_t st) {
+    return run_combine<float, D>(p, cu, partials, S, z, nullptr, mz, st);
   }
 };
 
@@ -876,8 +897,13 @@ gbla_status launch_conv(const Plan& p, const void* q, const void* k, const void*
 
 gbla_status launch_state(const Plan& p, const void* k, const void* v, const void* a,
                          const float* conv_w, const int32_t* cu, void* workspace, float* S,
-                         float* z, hipStream_t stream) {
-  return dispatch<StateRun>(p, k, v, a, conv_w, cu, workspace, S, z, stream);
+                         float* z, float* mz, hipStream_t stream) {
+  return dispatch<StateRun>(p, k, v, a, conv_w, cu, workspace, S, z, mz, stream);
+}
+
+gbla_status launch_combine_f32(const Plan& p, const int32_t* cu, const float* partials,
+                               float* S, float* z, float* mz, hipStream_t stream) {
+  return dispatch<CombineF32Run>(p, cu, partials, S, z, mz, stream);
 }
 
 gbla_status launch_readout(const Plan& p, const void* q, const void* r, const float* conv_w,

@@ -54,12 +54,41 @@ gbla_status make_plan(const gbla_shape* s, bool ragged, Plan* p);
 gbla_status launch_conv(const Plan& p, const void* q, const void* k, const void* v,
                         const float* conv_w, const int32_t* cu, float* qt, float* kt,
                         float* vt, hipStream_t stream);
+// S, z (normalised state) and mz (the softmax's max and sum per (sequence,
+// head)) are optional fp32 outputs; NULL skips them.
 gbla_status launch_state(const Plan& p, const void* k, const void* v, const void* a,
                          const float* conv_w, const int32_t* cu, void* workspace,
-                         float* S, float* z, hipStream_t stream);
+                         float* S, float* z, float* mz, hipStream_t stream);
 gbla_status launch_readout(const Plan& p, const void* q, const void* r, const float* conv_w,
                            const float* gamma, const int32_t* cu, const void* workspace,
                            float* out, hipStream_t stream);
+// The fixed-order combine of partial records [S_p | z_p | m_p | l_p] laid out
+// like the forward's (rec_floats apart, [H, units]), with full-accuracy expf
+// for every dtype and no readout operands: S, z, mz as in launch_state.
+gbla_status launch_combine_f32(const Plan& p, const int32_t* cu, const float* partials,
+                               float* S, float* z, float* mz, hipStream_t stream);
+
+// Workspace of the backward pass (bytes from the workspace base), all fp32.
+struct BwdLayout {
+  size_t off_S;     // [N, H, d, d] normalised state
+  size_t off_z;     // [N, H, d]
+  size_t off_mz;    // [N, H, 2] softmax max and sum of the gate logits
+  size_t off_dsp;   // [H, units, rec_floats] per-unit state partials, then
+                    // per-unit dS, dz partials
+  size_t off_dS;    // [N, H, d*d + d] dS, dz
+  size_t off_dgp;   // [H, units, d] per-unit dgamma partials
+  size_t off_dxt;   // [3, tokens * H * d] gradients of the convolved q, k, v
+  size_t off_dcp;   // [H, units, 3, d, 4] per-unit tap-gradient partials
+  size_t total_bytes;
+};
+BwdLayout make_bwd_layout(const Plan& p);
+
+// Backward launcher (gbla_backward.hip); dconv may be NULL (no Conv1D).
+gbla_status launch_backward(const Plan& p, const BwdLayout& L, const void* q, const void* k,
+                            const void* v, const void* a, const void* r, const float* conv_w,
+                            const float* gamma, const int32_t* cu, const float* dy, void* ws,
+                            float* dq, float* dk, float* dv, float* da, float* dr, float* dconv,
+                            float* dgamma, hipStream_t st);
 
 // Streaming kernels (gbla_stream.hip): bf16 inputs, head dim 32 or 64.
 bool stream_supported(const Plan& p);

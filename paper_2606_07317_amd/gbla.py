@@ -67,6 +67,10 @@ def load_library(path: str = LIB_PATH):
     lib.gbla_state.restype = ctypes.c_int
     lib.gbla_readout.argtypes = [SP, P, P, P, P, P, P, sz, P, P]
     lib.gbla_readout.restype = ctypes.c_int
+    lib.gbla_backward_workspace_bytes.argtypes = [SP]
+    lib.gbla_backward_workspace_bytes.restype = sz
+    lib.gbla_backward.argtypes = [SP, P, P, P, P, P, P, P, P, P, P, sz, P, P, P, P, P, P, P, P]
+    lib.gbla_backward.restype = ctypes.c_int
     lib.gbla_status_string.argtypes = [ctypes.c_int]
     lib.gbla_status_string.restype = ctypes.c_char_p
     if path == LIB_PATH:
@@ -240,3 +244,37 @@ def readout(q, out_gate, conv_w, norm_w, workspace, eps: float = 1e-6, cu_seqlen
                                      workspace.numel(), _ptr(out), _stream(stream))
     _raise(st, "gbla_readout")
     return out
+
+
+def backward_workspace_bytes(shape: Shape) -> int:
+    n = load_library().gbla_backward_workspace_bytes(ctypes.byref(shape))
+    if n == 0:
+        raise GblaError(1, "gbla_backward_workspace_bytes")
+    return int(n)
+
+
+def backward(q, k, v, gate_logits, out_gate, conv_w, norm_w, dy, eps: float = 1e-6,
+             cu_seqlens=None, max_seqlen=None, workspace=None, stream=None) -> dict:
+    """Gradients of sum(forward(...) * dy) with respect to every input (fp32):
+    a dict with dq, dk, dv, da (gate logits), dr (out gate), dconv_w, dgamma
+    (norm weight), shaped like the inputs."""
+    _check_inputs(q, k, v, gate_logits, out_gate, conv_w, norm_w, cu_seqlens)
+    dev = q.device
+    _check(dy, "dy", torch.float32, dev)
+    if dy.shape != q.shape:
+        raise ValueError("dy must have the shape of q")
+    shape = make_shape(q, conv_w, eps, cu_seqlens, max_seqlen, 0)
+    if workspace is None:
+        workspace = torch.empty(backward_workspace_bytes(shape), dtype=torch.uint8, device=dev)
+    f32 = dict(dtype=torch.float32, device=dev)
+    g = {n: torch.empty(q.shape, **f32) for n in ("dq", "dk", "dv", "dr")}
+    g["da"] = torch.empty(q.shape[:-1], **f32)
+    g["dconv_w"] = torch.empty(conv_w.shape, **f32)
+    g["dgamma"] = torch.empty(norm_w.shape, **f32)
+    st = load_library().gbla_backward(
+        ctypes.byref(shape), _ptr(q), _ptr(k), _ptr(v), _ptr(gate_logits), _ptr(out_gate),
+        _ptr(conv_w), _ptr(norm_w), _ptr(cu_seqlens), _ptr(dy), _ptr(workspace), workspace.numel(),
+        _ptr(g["dq"]), _ptr(g["dk"]), _ptr(g["dv"]), _ptr(g["da"]), _ptr(g["dr"]),
+        _ptr(g["dconv_w"]), _ptr(g["dgamma"]), _stream(stream))
+    _raise(st, "gbla_backward")
+    return g

@@ -178,6 +178,13 @@ def make_inputs(w: Workload | str, lengths: Optional[np.ndarray] = None) -> Inpu
     return Inputs(w, q, k, v, a, r, conv_w, gamma, cu_seqlens, w.eps)
 
 
+def make_cotangent(inp: Inputs, seed_offset: int = 1000) -> np.ndarray:
+    """Seeded dL/dy for a backward test: fp32 standard normal in the layout of
+    ``q``, from its own generator (seed = workload seed + ``seed_offset``)."""
+    rng = np.random.Generator(np.random.PCG64(inp.workload.seed + seed_offset))
+    return rng.standard_normal(size=inp.q.shape, dtype=np.float32)
+
+
 def to_f64(x: np.ndarray, dtype: str) -> np.ndarray:
     """Exact fp64 view of an activation array stored as ``dtype``."""
     if dtype == BF16:

@@ -27,7 +27,8 @@ def shape(**kw):
 def test_exports_every_declared_function(lib):
     names = gbla.declared_functions()
     assert {"gbla_forward", "gbla_workspace_bytes", "gbla_conv1d", "gbla_state",
-            "gbla_readout", "gbla_status_string"} <= set(names)
+            "gbla_readout", "gbla_status_string", "gbla_backward",
+            "gbla_backward_workspace_bytes"} <= set(names)
     for n in names:
         assert hasattr(lib, n), n
 
@@ -126,3 +127,37 @@ def test_ablation_switches_validation(lib):
                             None, 0, P, None) == 4
     assert lib.gbla_conv1d(ctypes.byref(shape(flags=gbla.NO_CONV, head_dim=16)), P, P, P, None,
                            None, P, P, P, None) == 2
+
+
+def _backward(lib, s, ws_bytes=None, **ptrs):
+    P = ALIGNED
+    p = dict(q=P, k=P, v=P, a=P, r=P, w=P, g=P, cu=None, dy=P, ws=P, dq=P, dk=P, dv=P, da=P,
+             dr=P, dw=P, dg=P)
+    p.update(ptrs)
+    if ws_bytes is None:
+        ws_bytes = lib.gbla_backward_workspace_bytes(ctypes.byref(s))
+    return lib.gbla_backward(ctypes.byref(s), p["q"], p["k"], p["v"], p["a"], p["r"], p["w"],
+                             p["g"], p["cu"], p["dy"], p["ws"], ws_bytes, p["dq"], p["dk"],
+                             p["dv"], p["da"], p["dr"], p["dw"], p["dg"], None)
+
+
+def test_backward_workspace_and_validation(lib):
+    s = shape()
+    bwd = lib.gbla_backward_workspace_bytes(ctypes.byref(s))
+    # three fp32 activation-sized buffers at least
+    assert bwd % 256 == 0 and bwd >= 3 * 8 * 32768 * 64 * 4
+    assert lib.gbla_backward_workspace_bytes(ctypes.byref(shape(head_dim=48))) == 0
+    assert lib.gbla_backward_workspace_bytes(None) == 0
+    for name in ("q", "k", "v", "a", "r", "w", "g", "dy", "dq", "dk", "dv", "da", "dr", "dw",
+                 "dg"):
+        assert _backward(lib, s, **{name: None}) == 1, name
+    for name in ("q", "dy", "dq", "dr", "w", "g", "dw", "dg"):
+        assert _backward(lib, s, **{name: MIS}) == 3, name
+    assert _backward(lib, s, da=ALIGNED + 2) == 3      # fp32 gradient of the logits
+    assert _backward(lib, s, ws=None) == 4
+    assert _backward(lib, s, ws=ALIGNED + 64) == 3
+    assert _backward(lib, s, ws_bytes=3 * 8 * 32768 * 64 * 4) == 4   # the dq~, dk~, dv~ buffers alone
+    assert _backward(lib, shape(head_dim=16)) == 2
+    for flags in (gbla.NO_GATE, gbla.NO_CONV, gbla.NO_NORM, gbla.BLA):
+        assert _backward(lib, shape(flags=flags)) == 2
+    assert _backward(lib, shape(flags=8)) == 1
