@@ -88,6 +88,67 @@ def cpu_baseline(inp, seconds: float):
                       % (inp.workload.name, inp.tokens, inp.workload.heads, len(times), med)}
 
 
+BWD_METRIC = "GBLA bwd tokens/sec at n=32768,H=8,d=64"
+
+
+def bench_backward(args, inp, dev):
+    """A step is one gbla_backward call (state recompute, query, key and
+    Conv1D passes, parameter-gradient sums) on resident inputs and dy."""
+    import torch
+    from paper_2606_07317_amd import gbla, inputs
+    w = inp.workload
+    base = inputs.device_tensors(inp, dev)
+    dy = torch.from_numpy(inputs.make_cotangent(inp)).to(dev)
+    shape = gbla.make_shape(base["q"], base["conv_w"], inp.eps, base["cu_seqlens"], base["max_seqlen"])
+    ws = torch.empty(gbla.backward_workspace_bytes(shape), dtype=torch.uint8, device=dev)
+    per_set = sum(base[n].numel() * base[n].element_size() for n in ("q", "k", "v", "a", "r"))
+    per_set += base["q"].numel() * 4 * 5 + base["a"].numel() * 4
+    nsets = args.sets or max(2, -(-(1 << 30) // per_set) + 1)
+    sets = []
+    for i in range(nsets):
+        t = {n: (base[n].clone() if isinstance(base[n], torch.Tensor) else base[n]) for n in base}
+        t["dy"] = dy.clone()
+        t["grads"] = gbla.backward(t["q"], t["k"], t["v"], t["a"], t["r"], t["conv_w"], t["gamma"],
+                                   t["dy"], eps=inp.eps, cu_seqlens=t["cu_seqlens"],
+                                   max_seqlen=t["max_seqlen"], workspace=ws)
+        sets.append(t)
+
+    def step(i):
+        t = sets[i % nsets]
+        gbla.backward(t["q"], t["k"], t["v"], t["a"], t["r"], t["conv_w"], t["gamma"], t["dy"],
+                      eps=inp.eps, cu_seqlens=t["cu_seqlens"], max_seqlen=t["max_seqlen"],
+                      workspace=ws, grads=t["grads"])
+
+    for i in range(args.warmup):
+        step(i)
+    stream = torch.cuda.current_stream()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for i in range(args.steps):
+        step(i)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms = ev0.elapsed_time(ev1) / args.steps
+    e = 2 if w.dtype == "bf16" else 4
+    d = w.head_dim
+    # inputs q, k, v, a, r and dy read once; dq, dk, dv, dr, da written once
+    byt = inp.tokens * w.heads * ((4 * d + 1) * e + 4 * d + 4 * (4 * d + 1))
+    gbps = byt / (ms * 1e-3) / 1e9
+    res = {"metric": BWD_METRIC, "value": inp.tokens / (ms * 1e-3), "unit": "tokens/s",
+           "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+           "dtype": "f32", "data": "synthetic",
+           "config": {"workload": w.name, "B": inp.nseq, "H": w.heads, "tokens": inp.tokens,
+                      "d": d, "conv_width": w.conv_width, "inputs": w.dtype, "pass": "backward",
+                      "rotating_sets": nsets, "algorithmic_bytes": byt,
+                      "effective_GBps": round(gbps, 1), "hbm_frac": round(gbps / HBM_PEAK_GBPS, 4),
+                      "wall_s": round(wall, 4)}}
+    print(json.dumps(res), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -97,6 +158,8 @@ def main():
     ap.add_argument("--sets", type=int, default=0, help="rotated input sets (0: enough for 1 GiB)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--pass", dest="which", choices=("forward", "backward"), default="forward",
+                    help="forward (the headline metric) or the backward pass (gbla_backward)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only copy 256 MiB device-to-device --steps times (reference for "
                          "rocprofv3 FETCH_SIZE / WRITE_SIZE scaling)")
@@ -124,6 +187,8 @@ def main():
         print(json.dumps({"calibrate_copy_bytes_each_way": 4 * n, "copies": args.steps}))
         return
     wname = args.workload or inputs.THROUGHPUT_WORKLOAD
+    if args.which == "backward":
+        return bench_backward(args, inputs.make_inputs(wname), dev)
     inp = inputs.make_inputs(wname)
     w = inp.workload
     base = inputs.device_tensors(inp, dev)

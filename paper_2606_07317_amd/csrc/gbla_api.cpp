@@ -94,6 +94,22 @@ gbla_status make_plan(const gbla_shape* s, bool ragged, Plan* p) {
   return GBLA_OK;
 }
 
+Plan backward_plan(const Plan& p) {
+  // Units of 256 tokens: the backward's workgroups carry more work per token
+  // than the forward's and need more of them in flight.
+  Plan b = p;
+  b.chunk = 256;
+  if (p.ragged) {
+    b.units = (int32_t)(b.tokens / b.chunk + b.nseq);
+  } else {
+    int64_t cps = ((int64_t)b.rows + b.chunk - 1) / b.chunk;
+    if (cps < 1) cps = 1;
+    b.chunks_per_seq = (int32_t)cps;
+    b.units = (int32_t)(cps * b.nseq);
+  }
+  return b;
+}
+
 BwdLayout make_bwd_layout(const Plan& p) {
   BwdLayout L{};
   const size_t pairs = (size_t)p.nseq * p.heads, d = p.d, f = sizeof(float);
@@ -250,8 +266,8 @@ size_t gbla_backward_workspace_bytes(const gbla_shape* shape) {
   Plan dense, ragged;
   if (gbla::make_plan(shape, false, &dense) != GBLA_OK) return 0;
   if (gbla::make_plan(shape, true, &ragged) != GBLA_OK) return 0;
-  const size_t a = gbla::make_bwd_layout(dense).total_bytes;
-  const size_t b = gbla::make_bwd_layout(ragged).total_bytes;
+  const size_t a = gbla::make_bwd_layout(gbla::backward_plan(dense)).total_bytes;
+  const size_t b = gbla::make_bwd_layout(gbla::backward_plan(ragged)).total_bytes;
   return a > b ? a : b;
 }
 
@@ -261,9 +277,10 @@ gbla_status gbla_backward(const gbla_shape* shape, const void* q, const void* k,
                           void* workspace, size_t workspace_bytes, float* dq, float* dk,
                           float* dv, float* d_gate_logits, float* d_out_gate, float* d_conv_w,
                           float* d_norm_w, void* stream) {
-  Plan p;
-  GBLA_TRY(gbla::make_plan(shape, cu_seqlens != nullptr, &p));
-  if (p.flags != 0) return GBLA_ERR_UNSUPPORTED;
+  Plan p0;
+  GBLA_TRY(gbla::make_plan(shape, cu_seqlens != nullptr, &p0));
+  if (p0.flags != 0) return GBLA_ERR_UNSUPPORTED;
+  const Plan p = gbla::backward_plan(p0);
   GBLA_TRY(check_acts(p, {q, k, v, out_gate, dy, dq, dk, dv, d_out_gate}));
   GBLA_TRY(check_used({conv_w, norm_w, d_conv_w, d_norm_w}));
   GBLA_TRY(check_logits(p, gate_logits));

@@ -81,6 +81,9 @@ struct BwdLayout {
   size_t off_dcp;   // [H, units, 3, d, 4] per-unit tap-gradient partials
   size_t total_bytes;
 };
+// The backward's plan: the forward's with its own unit size (the state
+// partials, dS partials and tap partials are per unit of this plan).
+Plan backward_plan(const Plan& p);
 BwdLayout make_bwd_layout(const Plan& p);
 
 // Backward launcher (gbla_backward.hip); dconv may be NULL (no Conv1D).

@@ -254,10 +254,12 @@ def backward_workspace_bytes(shape: Shape) -> int:
 
 
 def backward(q, k, v, gate_logits, out_gate, conv_w, norm_w, dy, eps: float = 1e-6,
-             cu_seqlens=None, max_seqlen=None, workspace=None, stream=None) -> dict:
+             cu_seqlens=None, max_seqlen=None, workspace=None, stream=None,
+             grads: Optional[dict] = None) -> dict:
     """Gradients of sum(forward(...) * dy) with respect to every input (fp32):
     a dict with dq, dk, dv, da (gate logits), dr (out gate), dconv_w, dgamma
-    (norm weight), shaped like the inputs."""
+    (norm weight), shaped like the inputs.  ``grads`` may hold preallocated
+    fp32 outputs under those names; they are overwritten."""
     _check_inputs(q, k, v, gate_logits, out_gate, conv_w, norm_w, cu_seqlens)
     dev = q.device
     _check(dy, "dy", torch.float32, dev)
@@ -267,10 +269,15 @@ def backward(q, k, v, gate_logits, out_gate, conv_w, norm_w, dy, eps: float = 1e
     if workspace is None:
         workspace = torch.empty(backward_workspace_bytes(shape), dtype=torch.uint8, device=dev)
     f32 = dict(dtype=torch.float32, device=dev)
-    g = {n: torch.empty(q.shape, **f32) for n in ("dq", "dk", "dv", "dr")}
-    g["da"] = torch.empty(q.shape[:-1], **f32)
-    g["dconv_w"] = torch.empty(conv_w.shape, **f32)
-    g["dgamma"] = torch.empty(norm_w.shape, **f32)
+    want = {n: q.shape for n in ("dq", "dk", "dv", "dr")}
+    want.update(da=q.shape[:-1], dconv_w=conv_w.shape, dgamma=norm_w.shape)
+    g = dict(grads or {})
+    for n, shp in want.items():
+        if n not in g:
+            g[n] = torch.empty(shp, **f32)
+        _check(g[n], n, torch.float32, dev)
+        if g[n].shape != shp:
+            raise ValueError("%s must have shape %s" % (n, tuple(shp)))
     st = load_library().gbla_backward(
         ctypes.byref(shape), _ptr(q), _ptr(k), _ptr(v), _ptr(gate_logits), _ptr(out_gate),
         _ptr(conv_w), _ptr(norm_w), _ptr(cu_seqlens), _ptr(dy), _ptr(workspace), workspace.numel(),
