@@ -50,6 +50,12 @@ __device__ __forceinline__ void wave_lds_sync() {
 }
 
 __device__ __forceinline__ float phi_f(float u) { return u > 0.0f ? u + 1.0f : expf(u); }
+// Hardware-exp forms for the matrix-core kernels (a few ulp; the gradients
+// are held to fp32-sum accuracy, far above that).
+__device__ __forceinline__ float phi_fast(float u) { return u > 0.0f ? u + 1.0f : __expf(u); }
+__device__ __forceinline__ float sigmoid_fast(float x) {
+  return __builtin_amdgcn_rcpf(1.0f + __expf(-x));
+}
 __device__ __forceinline__ float dphi_f(float u) { return u > 0.0f ? 1.0f : expf(u); }
 
 template <int D>
@@ -620,7 +626,8 @@ bwd_param_kernel(Plan P, const int32_t* __restrict__ cu, const float* __restrict
 template <int D>
 struct MF {
   static constexpr int NMB = D / 16;          // 16-channel blocks
-  static constexpr int kRow = D + 4;          // staging row stride (floats)
+  // staging row stride (floats): the four lane groups' rows start 16 banks apart
+  static constexpr int kRow = D + 16;
   static constexpr int kStage = 16 * kRow;    // one wave's 16-token array
   static constexpr int kBlocks = NMB * NMB;   // 16x16 blocks of a d x d result
   static constexpr int kStep = 64;            // tokens between a wave's blocks
@@ -941,7 +948,7 @@ bwd_state_mfma_kernel(Plan P, const T* __restrict__ kin, const T* __restrict__ v
     __asm__ volatile("" ::: "memory");  // taps are re-read from LDS, not held
     sk.conv(tk, g, kt);
     sv.conv(tv, g, vt);
-    const float w = tok < t1 ? expf(al - m) : 0.0f;
+    const float w = tok < t1 ? __expf(al - m) : 0.0f;
     // the next block's rows (out of range past the slice: read as 0, unused)
     tok += 16;
     sk.issue(rk, tok, g);
@@ -952,7 +959,7 @@ bwd_state_mfma_kernel(Plan P, const T* __restrict__ kin, const T* __restrict__ v
     for (int kq = 0; kq < NMB; ++kq)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        kt[kq][i] = w * phi_f(kt[kq][i]);
+        kt[kq][i] = w * phi_fast(kt[kq][i]);
         zacc[kq][i] += kt[kq][i];
       }
     wave_lds_sync();  // the previous block's reads of X, Y are done
@@ -1077,7 +1084,7 @@ bwd_query_mfma_kernel(Plan P, const T* __restrict__ qin, const T* __restrict__ r
       const f32x4_t zr = *reinterpret_cast<const f32x4_t*>(&zs[16 * kq + 4 * g]);
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        qh[kq][i] = phi_f(qh[kq][i]);
+        qh[kq][i] = phi_fast(qh[kq][i]);
         zd = fmaf(qh[kq][i], zr[i], zd);
       }
     }
@@ -1105,7 +1112,7 @@ bwd_query_mfma_kernel(Plan P, const T* __restrict__ qin, const T* __restrict__ r
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const float r = rv[kq][i], d = dyv[kq][i];
-        const float sig = 1.0f / (1.0f + expf(-r)), silu = r * sig;
+        const float sig = sigmoid_fast(r), silu = r * sig;
         const float oh = o[kq][i] * rs;
         doh[kq][i] = d * gm[i] * silu;
         dgacc[kq][i] = fmaf(d * oh, silu, dgacc[kq][i]);
@@ -1225,7 +1232,7 @@ bwd_key_mfma_kernel(Plan P, const T* __restrict__ kin, const T* __restrict__ vin
     __asm__ volatile("" ::: "memory");
     sk.conv(tk, g, kt);
     sv.conv(tv, g, vt);
-    const float gj = expf(al - M) * invZ;
+    const float gj = __expf(al - M) * invZ;
     const int cur = tok;
     tok += 16;
     sk.issue(rk, tok, g);  // the next block's rows (out of range past the slice: 0, unused)
@@ -1244,7 +1251,7 @@ bwd_key_mfma_kernel(Plan P, const T* __restrict__ kin, const T* __restrict__ vin
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const float u = kt[kq][i];
-        const float p = phi_f(u);
+        const float p = phi_fast(u);
         const float t = acc4[kq][i] + dzr[i];
         dk[i] = gj * t * (u > 0.0f ? 1.0f : p);
         dgl = fmaf(p, t, dgl);
