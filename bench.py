@@ -149,6 +149,76 @@ def bench_backward(args, inp, dev):
     print(json.dumps(res), flush=True)
 
 
+# Per-layer latency of GBLA on H100 at batch 8 (the paper's Table 5), for context.
+PAPER_H100_LAYER_MS = {2048: 0.618, 4096: 1.141, 8192: 2.199, 16384: 4.266, 32768: 8.217}
+MFMA_BF16_PEAK_TFLOPS = 2500.0
+
+
+def bench_layer(args, inp, dev):
+    """A step is one gbla_layer_forward: the conv on the embeddings, the
+    stacked projections (bf16 MFMA GEMM) and the attention core."""
+    import torch
+    from paper_2606_07317_amd import gbla, inputs
+    w = inp.workload
+    base = inputs.layer_device_tensors(inp, dev)
+    shape = gbla.layer_shape(base["x"], base["conv_x"], w.heads, w.head_dim, w.eps)
+    ws = torch.empty(gbla.layer_workspace_bytes(shape), dtype=torch.uint8, device=dev)
+    per_set = base["x"].numel() * 2 + base["x"].shape[0] * w.heads * base["x"].shape[1] * w.head_dim * 4
+    nsets = args.sets or max(2, -(-(1 << 30) // per_set) + 1)
+    sets = []
+    for i in range(nsets):
+        x = base["x"].clone() if i else base["x"]
+        out = torch.empty((w.batch, w.heads, w.seqlen, w.head_dim), dtype=torch.float32, device=dev)
+        sets.append((x, out))
+
+    def step(i):
+        x, out = sets[i % nsets]
+        gbla.layer_forward(x, base["conv_x"], base["w_proj"], base["gamma"], eps=w.eps,
+                           workspace=ws, out=out)
+
+    for i in range(args.warmup):
+        step(i)
+    stream = torch.cuda.current_stream()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for i in range(args.steps):
+        step(i)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms = ev0.elapsed_time(ev1) / args.steps
+    # the projection GEMM alone, timed live on the same stream
+    pairs = []
+    for i in range(min(args.steps, 50)):
+        x, _ = sets[i % nsets]
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        gbla.layer_project(x, base["conv_x"], base["w_proj"], w.heads, w.head_dim)
+        b.record(stream)
+        pairs.append((a, b))
+    torch.cuda.synchronize()
+    proj_ms = statistics.mean(a.elapsed_time(b) for a, b in pairs)
+    tokens = w.batch * w.seqlen
+    flops = 2.0 * tokens * w.d_model * w.heads * (4 * w.head_dim + 1)
+    tfl = flops / (proj_ms * 1e-3) / 1e12
+    res = {"metric": "GBLA layer forward latency from the embeddings (Table 5 shape)",
+           "value": ms, "unit": "ms/layer", "n_gpus": 1, "steps": args.steps,
+           "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": False,
+           "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+           "config": {"workload": w.name, "B": w.batch, "L": w.seqlen, "d_model": w.d_model,
+                      "H": w.heads, "d": w.head_dim, "conv_width": w.conv_width,
+                      "tokens_per_s": tokens / (ms * 1e-3), "rotating_sets": nsets,
+                      "paper_h100_ms": PAPER_H100_LAYER_MS.get(w.seqlen),
+                      "wall_s": round(wall, 4)},
+           "roofline": {"bound": "mfma", "kernel": "proj_kernel", "achieved": round(tfl, 1),
+                        "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                        "frac": round(tfl / MFMA_BF16_PEAK_TFLOPS, 4), "avg_launch_ms": proj_ms,
+                        "traffic": None}}
+    print(json.dumps(res), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -158,8 +228,11 @@ def main():
     ap.add_argument("--sets", type=int, default=0, help="rotated input sets (0: enough for 1 GiB)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--pass", dest="which", choices=("forward", "backward"), default="forward",
-                    help="forward (the headline metric) or the backward pass (gbla_backward)")
+    ap.add_argument("--pass", dest="which", choices=("forward", "backward", "layer"),
+                    default="forward",
+                    help="forward (the headline metric), the backward pass (gbla_backward) or "
+                         "the full layer from the embeddings (gbla_layer_forward; --workload "
+                         "layer_b8_n2048 or layer_b8_n32768)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only copy 256 MiB device-to-device --steps times (reference for "
                          "rocprofv3 FETCH_SIZE / WRITE_SIZE scaling)")
@@ -186,6 +259,9 @@ def main():
         torch.cuda.synchronize()
         print(json.dumps({"calibrate_copy_bytes_each_way": 4 * n, "copies": args.steps}))
         return
+    if args.which == "layer":
+        return bench_layer(args, inputs.make_layer_inputs(
+            inputs.LAYER_WORKLOADS[args.workload or "layer_b8_n32768"]), dev)
     wname = args.workload or inputs.THROUGHPUT_WORKLOAD
     if args.which == "backward":
         return bench_backward(args, inputs.make_inputs(wname), dev)

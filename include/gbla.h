@@ -187,6 +187,56 @@ gbla_status gbla_backward(const gbla_shape* shape, const void* q, const void* k,
                           float* d_gate_logits, float* d_out_gate, float* d_conv_w,
                           float* d_norm_w, void* stream);
 
+/*
+ * The full GBLA layer from the input embeddings X (Section 2.1, the paper's
+ * own placement of the conv):
+ *   Xt = Conv1D(X)  (causal, depthwise over the d_model channels)
+ *   Q = Xt W_Q, K = Xt W_K, V = Xt W_V, a = Xt w_g, R = Xt W_R  (per head)
+ *   y  = the attention and gated RMSNorm of gbla_forward on (Q, K, V, a, R)
+ *        with no further conv.
+ * bf16 only: Xt and the projections are rounded to bf16 (fp32
+ * accumulation), as a bf16 layer stores them.
+ */
+typedef struct {
+  int32_t batch;      /* B (dense) or N_s (ragged)                              */
+  int32_t seqlen;     /* L (dense) or T = cu_seqlens[N_s] (ragged), >= 0         */
+  int32_t d_model;    /* model width: a multiple of 64, at most 16384            */
+  int32_t heads;      /* H >= 1                                                  */
+  int32_t head_dim;   /* d in {32, 64, 128}                                      */
+  int32_t conv_width; /* W in [1, 4]                                             */
+  int32_t max_seqlen; /* ragged: an upper bound of the lengths; dense: 0         */
+  int32_t dtype;      /* GBLA_BF16                                               */
+  float eps;          /* RMSNorm epsilon                                         */
+} gbla_layer_shape;
+
+/* Scratch bytes of gbla_layer_forward (the projections and the core's
+ * workspace), for both the dense and the ragged reading; 0 if invalid. */
+size_t gbla_layer_workspace_bytes(const gbla_layer_shape* shape);
+
+/*
+ * The conv and the projections alone (test and stage hook):
+ *   x        [B, L, d_model] or [T, d_model] bf16 (token-major embeddings)
+ *   conv_x   [d_model, W] fp32, tap W-1 on the current token
+ *   w_proj   [4*H*d + H, d_model] bf16: the output features' weight rows,
+ *            W_Q's columns (h, e) at rows h*d + e, then W_K, W_V, W_R at
+ *            offsets H*d, 2*H*d, 3*H*d, then w_g's H columns
+ *   q, k, v, r  [B, H, L, d] or [H, T, d] bf16 outputs; a [B, H, L] or [H, T]
+ * Base pointers 16-byte aligned (a: 2 bytes).  Does not synchronize.
+ */
+gbla_status gbla_layer_project(const gbla_layer_shape* shape, const void* x,
+                               const float* conv_x, const void* w_proj,
+                               const int32_t* cu_seqlens, void* q, void* k, void* v,
+                               void* r, void* a, void* stream);
+
+/*
+ * The whole layer: out [B, H, L, d] or [H, T, d] fp32 (the layout of
+ * gbla_forward's output), norm_w [H, d] fp32 gamma.
+ */
+gbla_status gbla_layer_forward(const gbla_layer_shape* shape, const void* x,
+                               const float* conv_x, const void* w_proj, const float* norm_w,
+                               const int32_t* cu_seqlens, void* workspace,
+                               size_t workspace_bytes, float* out, void* stream);
+
 /* A static, human-readable name of a status code (never NULL). */
 const char* gbla_status_string(gbla_status status);
 

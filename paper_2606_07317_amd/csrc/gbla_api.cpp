@@ -110,6 +110,57 @@ Plan backward_plan(const Plan& p) {
   return b;
 }
 
+gbla_status make_layer_plan(const gbla_layer_shape* s, bool ragged, LayerPlan* p) {
+  if (!s || !p) return GBLA_ERR_INVALID_ARGUMENT;
+  if (s->batch < 1 || s->heads < 1 || s->seqlen < 0) return GBLA_ERR_INVALID_ARGUMENT;
+  if (s->dtype != GBLA_BF16) return GBLA_ERR_UNSUPPORTED;
+  if (s->d_model < 64 || s->d_model > 16384 || s->d_model % 64 != 0) return GBLA_ERR_UNSUPPORTED;
+  if (s->conv_width < 1 || s->conv_width > 4) return GBLA_ERR_UNSUPPORTED;
+  LayerPlan L{};
+  L.nseq = s->batch;
+  L.rows = s->seqlen;
+  L.d_model = s->d_model;
+  L.heads = s->heads;
+  L.d = s->head_dim;
+  L.W = s->conv_width;
+  L.ragged = ragged ? 1 : 0;
+  const int64_t tokens = ragged ? (int64_t)s->seqlen : (int64_t)s->batch * s->seqlen;
+  const int64_t features = (int64_t)s->heads * (4 * (int64_t)s->head_dim + 1);
+  // 32-bit buffer offsets over X and the weights
+  if (tokens * s->d_model * 2 >= (int64_t(1) << 31)) return GBLA_ERR_UNSUPPORTED;
+  if (features * s->d_model * 2 >= (int64_t(1) << 31)) return GBLA_ERR_UNSUPPORTED;
+  L.tokens = (int32_t)tokens;
+  L.features = (int32_t)features;
+  gbla_shape cs{};
+  cs.batch = s->batch;
+  cs.heads = s->heads;
+  cs.seqlen = s->seqlen;
+  cs.head_dim = s->head_dim;
+  cs.conv_width = 1;
+  cs.max_seqlen = ragged ? s->max_seqlen : 0;
+  cs.dtype = GBLA_BF16;
+  cs.eps = s->eps;
+  cs.flags = GBLA_NO_CONV;
+  gbla_status st = make_plan(&cs, ragged, &L.core);
+  if (st != GBLA_OK) return st;
+  const size_t act = (size_t)tokens * s->heads * s->head_dim * 2;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off = align_up(off + bytes, 256);
+    return at;
+  };
+  L.off_q = take(act);
+  L.off_k = take(act);
+  L.off_v = take(act);
+  L.off_r = take(act);
+  L.off_a = take((size_t)tokens * s->heads * 2);
+  L.off_core = take(L.core.total_bytes);
+  L.total_bytes = off;
+  *p = L;
+  return GBLA_OK;
+}
+
 BwdLayout make_bwd_layout(const Plan& p) {
   BwdLayout L{};
   const size_t pairs = (size_t)p.nseq * p.heads, d = p.d, f = sizeof(float);
@@ -293,6 +344,45 @@ gbla_status gbla_backward(const gbla_shape* shape, const void* q, const void* k,
   return gbla::launch_backward(p, L, q, k, v, gate_logits, out_gate, conv_w, norm_w, cu_seqlens,
                                dy, workspace, dq, dk, dv, d_gate_logits, d_out_gate, d_conv_w,
                                d_norm_w, static_cast<hipStream_t>(stream));
+}
+
+size_t gbla_layer_workspace_bytes(const gbla_layer_shape* shape) {
+  gbla::LayerPlan dense, ragged;
+  if (gbla::make_layer_plan(shape, false, &dense) != GBLA_OK) return 0;
+  if (gbla::make_layer_plan(shape, true, &ragged) != GBLA_OK) return 0;
+  return dense.total_bytes > ragged.total_bytes ? dense.total_bytes : ragged.total_bytes;
+}
+
+gbla_status gbla_layer_project(const gbla_layer_shape* shape, const void* x, const float* conv_x,
+                               const void* w_proj, const int32_t* cu_seqlens, void* q, void* k,
+                               void* v, void* r, void* a, void* stream) {
+  gbla::LayerPlan L;
+  GBLA_TRY(gbla::make_layer_plan(shape, cu_seqlens != nullptr, &L));
+  GBLA_TRY(check_used({x, conv_x, w_proj, q, k, v, r}));
+  if (!a) return GBLA_ERR_INVALID_ARGUMENT;
+  if (!gbla::aligned(a, 2)) return GBLA_ERR_MISALIGNED;
+  return gbla::launch_project(L, x, conv_x, w_proj, cu_seqlens, q, k, v, r, a,
+                              static_cast<hipStream_t>(stream));
+}
+
+gbla_status gbla_layer_forward(const gbla_layer_shape* shape, const void* x, const float* conv_x,
+                               const void* w_proj, const float* norm_w,
+                               const int32_t* cu_seqlens, void* workspace, size_t workspace_bytes,
+                               float* out, void* stream) {
+  gbla::LayerPlan L;
+  GBLA_TRY(gbla::make_layer_plan(shape, cu_seqlens != nullptr, &L));
+  GBLA_TRY(check_used({x, conv_x, w_proj, norm_w, out}));
+  if (!workspace) return GBLA_ERR_WORKSPACE;
+  if (!gbla::aligned(workspace, 256)) return GBLA_ERR_MISALIGNED;
+  if (workspace_bytes < L.total_bytes) return GBLA_ERR_WORKSPACE;
+  unsigned char* ws = static_cast<unsigned char*>(workspace);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  void *q = ws + L.off_q, *k = ws + L.off_k, *v = ws + L.off_v, *r = ws + L.off_r, *a = ws + L.off_a;
+  GBLA_TRY(gbla::launch_project(L, x, conv_x, w_proj, cu_seqlens, q, k, v, r, a, st));
+  void* cws = ws + L.off_core;
+  GBLA_TRY(gbla::launch_state(L.core, k, v, a, nullptr, cu_seqlens, cws, nullptr, nullptr,
+                              nullptr, st));
+  return gbla::launch_readout(L.core, q, r, nullptr, norm_w, cu_seqlens, cws, out, st);
 }
 
 const char* gbla_status_string(gbla_status status) {

@@ -93,6 +93,26 @@ gbla_status launch_backward(const Plan& p, const BwdLayout& L, const void* q, co
                             float* dq, float* dk, float* dv, float* da, float* dr, float* dconv,
                             float* dgamma, hipStream_t st);
 
+// The full layer from X (gbla_layer.hip): the conv on X and the stacked
+// projections, then the attention core with its own conv switched off.
+struct LayerPlan {
+  int32_t nseq;       // B or N_s
+  int32_t rows;       // L (dense) or T (ragged)
+  int32_t d_model;
+  int32_t heads;
+  int32_t d;
+  int32_t W;
+  int32_t ragged;
+  int32_t tokens;     // B * L or T
+  int32_t features;   // 4 * H * d + H, the rows of the stacked projection weights
+  Plan core;          // plan of the attention core (flags GBLA_NO_CONV)
+  size_t off_q, off_k, off_v, off_r, off_a, off_core, total_bytes;
+};
+gbla_status make_layer_plan(const gbla_layer_shape* s, bool ragged, LayerPlan* p);
+gbla_status launch_project(const LayerPlan& p, const void* x, const float* conv_x,
+                           const void* w_proj, const int32_t* cu, void* q, void* k, void* v,
+                           void* r, void* a, hipStream_t stream);
+
 // Streaming kernels (gbla_stream.hip): bf16 inputs, head dim 32 or 64.
 bool stream_supported(const Plan& p);
 gbla_status launch_state_stream(const Plan& p, const void* k, const void* v, const void* a,

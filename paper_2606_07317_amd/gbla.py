@@ -43,6 +43,13 @@ class Shape(ctypes.Structure):
                 ("flags", ctypes.c_uint32)]
 
 
+class LayerShape(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("seqlen", ctypes.c_int32), ("d_model", ctypes.c_int32),
+                ("heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("conv_width", ctypes.c_int32), ("max_seqlen", ctypes.c_int32),
+                ("dtype", ctypes.c_int32), ("eps", ctypes.c_float)]
+
+
 _lib = None
 
 
@@ -71,6 +78,13 @@ def load_library(path: str = LIB_PATH):
     lib.gbla_backward_workspace_bytes.restype = sz
     lib.gbla_backward.argtypes = [SP, P, P, P, P, P, P, P, P, P, P, sz, P, P, P, P, P, P, P, P]
     lib.gbla_backward.restype = ctypes.c_int
+    LP = ctypes.POINTER(LayerShape)
+    lib.gbla_layer_workspace_bytes.argtypes = [LP]
+    lib.gbla_layer_workspace_bytes.restype = sz
+    lib.gbla_layer_project.argtypes = [LP, P, P, P, P, P, P, P, P, P, P]
+    lib.gbla_layer_project.restype = ctypes.c_int
+    lib.gbla_layer_forward.argtypes = [LP, P, P, P, P, P, P, sz, P, P]
+    lib.gbla_layer_forward.restype = ctypes.c_int
     lib.gbla_status_string.argtypes = [ctypes.c_int]
     lib.gbla_status_string.restype = ctypes.c_char_p
     if path == LIB_PATH:
@@ -285,3 +299,84 @@ def backward(q, k, v, gate_logits, out_gate, conv_w, norm_w, dy, eps: float = 1e
         _ptr(g["dconv_w"]), _ptr(g["dgamma"]), _stream(stream))
     _raise(st, "gbla_backward")
     return g
+
+
+# ---------------------------------------------------------------------------
+# The full layer from the embeddings X.
+# ---------------------------------------------------------------------------
+def layer_shape(x, conv_x, heads: int, head_dim: int, eps: float, cu_seqlens=None,
+                max_seqlen=None) -> LayerShape:
+    if cu_seqlens is None:
+        if x.dim() != 3:
+            raise ValueError("dense x must be [B, L, d_model]")
+        B, L, dm = x.shape
+        batch, rows, msl = B, L, 0
+    else:
+        if x.dim() != 2:
+            raise ValueError("ragged x must be [T, d_model]")
+        rows, dm = x.shape
+        batch = cu_seqlens.numel() - 1
+        msl = int(max_seqlen) if max_seqlen is not None else rows
+    if conv_x.dim() != 2 or conv_x.shape[0] != dm:
+        raise ValueError("conv_x must be [d_model, W]")
+    return LayerShape(batch, rows, dm, heads, head_dim, conv_x.shape[1], msl, _dtype_code(x),
+                      float(eps))
+
+
+def _check_layer(x, conv_x, w_proj, heads, head_dim, cu_seqlens):
+    dev = x.device
+    _check(x, "x", torch.bfloat16, dev)
+    _check(conv_x, "conv_x", torch.float32, dev)
+    _check(w_proj, "w_proj", torch.bfloat16, dev)
+    if w_proj.shape != (heads * (4 * head_dim + 1), x.shape[-1]):
+        raise ValueError("w_proj must be [H*(4*d+1), d_model]")
+    if cu_seqlens is not None:
+        _check(cu_seqlens, "cu_seqlens", torch.int32, dev)
+
+
+def layer_project(x, conv_x, w_proj, heads: int, head_dim: int, cu_seqlens=None,
+                  max_seqlen=None, stream=None) -> dict:
+    """Conv1D on x and the stacked projections: bf16 q, k, v, r in the
+    attention layout ([B,H,L,d] or [H,T,d]) and the gate logits a."""
+    _check_layer(x, conv_x, w_proj, heads, head_dim, cu_seqlens)
+    shape = layer_shape(x, conv_x, heads, head_dim, 0.0, cu_seqlens, max_seqlen)
+    if cu_seqlens is None:
+        act = (shape.batch, heads, shape.seqlen, head_dim)
+    else:
+        act = (heads, shape.seqlen, head_dim)
+    out = {n: torch.empty(act, dtype=torch.bfloat16, device=x.device) for n in ("q", "k", "v", "r")}
+    out["a"] = torch.empty(act[:-1], dtype=torch.bfloat16, device=x.device)
+    st = load_library().gbla_layer_project(
+        ctypes.byref(shape), _ptr(x), _ptr(conv_x), _ptr(w_proj), _ptr(cu_seqlens), _ptr(out["q"]),
+        _ptr(out["k"]), _ptr(out["v"]), _ptr(out["r"]), _ptr(out["a"]), _stream(stream))
+    _raise(st, "gbla_layer_project")
+    return out
+
+
+def layer_workspace_bytes(shape: LayerShape) -> int:
+    n = load_library().gbla_layer_workspace_bytes(ctypes.byref(shape))
+    if n == 0:
+        raise GblaError(1, "gbla_layer_workspace_bytes")
+    return int(n)
+
+
+def layer_forward(x, conv_x, w_proj, norm_w, eps: float = 1e-6, cu_seqlens=None,
+                  max_seqlen=None, workspace=None, out=None, stream=None) -> torch.Tensor:
+    """The whole layer from the embeddings x; y in the attention layout."""
+    if norm_w.dim() != 2:
+        raise ValueError("norm_w must be [H, d]")
+    heads, head_dim = norm_w.shape
+    _check_layer(x, conv_x, w_proj, heads, head_dim, cu_seqlens)
+    _check(norm_w, "norm_w", torch.float32, x.device)
+    shape = layer_shape(x, conv_x, heads, head_dim, eps, cu_seqlens, max_seqlen)
+    if workspace is None:
+        workspace = torch.empty(layer_workspace_bytes(shape), dtype=torch.uint8, device=x.device)
+    if out is None:
+        act = ((shape.batch, heads, shape.seqlen, head_dim) if cu_seqlens is None
+               else (heads, shape.seqlen, head_dim))
+        out = torch.empty(act, dtype=torch.float32, device=x.device)
+    st = load_library().gbla_layer_forward(
+        ctypes.byref(shape), _ptr(x), _ptr(conv_x), _ptr(w_proj), _ptr(norm_w), _ptr(cu_seqlens),
+        _ptr(workspace), workspace.numel(), _ptr(out), _stream(stream))
+    _raise(st, "gbla_layer_forward")
+    return out

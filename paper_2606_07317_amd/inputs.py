@@ -185,6 +185,83 @@ def make_cotangent(inp: Inputs, seed_offset: int = 1000) -> np.ndarray:
     return rng.standard_normal(size=inp.q.shape, dtype=np.float32)
 
 
+@dataclasses.dataclass(frozen=True)
+class LayerWorkload:
+    """A full-layer batch: embeddings X [B, L, d_model] (or packed [T, d_model])."""
+    name: str
+    batch: int
+    seqlen: int           # L (dense); ignored for ragged
+    d_model: int
+    heads: int
+    head_dim: int
+    conv_width: int
+    seed: int
+    ragged: bool = False
+    eps: float = 1e-6
+
+    def with_(self, **kw) -> "LayerWorkload":
+        return dataclasses.replace(self, **kw)
+
+
+# Table 5's layer (batch 8, model width 1024, 16 heads of 64) at two lengths.
+LAYER_WORKLOADS = {
+    "layer_b8_n2048": LayerWorkload("layer_b8_n2048", batch=8, seqlen=2048, d_model=1024, heads=16,
+                                    head_dim=64, conv_width=4, seed=5),
+    "layer_b8_n32768": LayerWorkload("layer_b8_n32768", batch=8, seqlen=32768, d_model=1024,
+                                     heads=16, head_dim=64, conv_width=4, seed=6),
+}
+
+
+@dataclasses.dataclass
+class LayerInputs:
+    workload: LayerWorkload
+    x: np.ndarray          # uint16 bf16 bits, [B, L, d_model] or [T, d_model]
+    conv_x: np.ndarray     # float32 [d_model, W]
+    w_proj: np.ndarray     # uint16 bf16 bits, [4*H*d + H, d_model]
+    gamma: np.ndarray      # float32 [H, d]
+    cu_seqlens: Optional[np.ndarray]
+
+
+def make_layer_inputs(w: LayerWorkload, lengths=None) -> LayerInputs:
+    """Draw order from PCG64(seed): lengths (ragged only), x, conv noise,
+    weights, gamma noise.  x ~ N(0, 1) and the weights ~ N(0, 1/d_model), both
+    rounded once to bf16, so every projection is about N(0, 1); taps are
+    0.1 N(0, 1) plus 1 on the current token; gamma is 1 + 0.1 N(0, 1)."""
+    rng = np.random.Generator(np.random.PCG64(w.seed))
+    if w.ragged:
+        lengths = np.asarray(lengths, dtype=np.int64)
+        cu = np.zeros(len(lengths) + 1, dtype=np.int64)
+        np.cumsum(lengths, out=cu[1:])
+        cu_seqlens = cu.astype(np.int32)
+        xs = (int(cu[-1]), w.d_model)
+        if len(lengths) != w.batch:
+            w = w.with_(batch=len(lengths))
+    else:
+        cu_seqlens = None
+        xs = (w.batch, w.seqlen, w.d_model)
+    x = f32_to_bf16_bits(rng.standard_normal(size=xs, dtype=np.float32))
+    conv_x = (0.1 * rng.standard_normal(size=(w.d_model, w.conv_width), dtype=np.float32)).astype(np.float32)
+    conv_x[:, -1] += np.float32(1.0)
+    N = w.heads * (4 * w.head_dim + 1)
+    wp = rng.standard_normal(size=(N, w.d_model), dtype=np.float32) / np.float32(np.sqrt(w.d_model))
+    w_proj = f32_to_bf16_bits(wp.astype(np.float32))
+    gamma = (np.float32(1.0) + np.float32(0.1) * rng.standard_normal(size=(w.heads, w.head_dim),
+                                                                      dtype=np.float32)).astype(np.float32)
+    return LayerInputs(w, x, conv_x, w_proj, gamma, cu_seqlens)
+
+
+def layer_device_tensors(inp: LayerInputs, device) -> dict:
+    import torch
+    out = {"x": to_torch(inp.x, BF16, device), "w_proj": to_torch(inp.w_proj, BF16, device),
+           "conv_x": torch.from_numpy(np.ascontiguousarray(inp.conv_x)).to(device),
+           "gamma": torch.from_numpy(np.ascontiguousarray(inp.gamma)).to(device)}
+    out["cu_seqlens"] = (torch.from_numpy(inp.cu_seqlens).to(device)
+                         if inp.cu_seqlens is not None else None)
+    out["max_seqlen"] = (int(np.diff(inp.cu_seqlens).max()) if inp.cu_seqlens is not None
+                         and len(inp.cu_seqlens) > 1 else None)
+    return out
+
+
 def to_f64(x: np.ndarray, dtype: str) -> np.ndarray:
     """Exact fp64 view of an activation array stored as ``dtype``."""
     if dtype == BF16:

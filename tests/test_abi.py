@@ -28,7 +28,8 @@ def test_exports_every_declared_function(lib):
     names = gbla.declared_functions()
     assert {"gbla_forward", "gbla_workspace_bytes", "gbla_conv1d", "gbla_state",
             "gbla_readout", "gbla_status_string", "gbla_backward",
-            "gbla_backward_workspace_bytes"} <= set(names)
+            "gbla_backward_workspace_bytes", "gbla_layer_workspace_bytes", "gbla_layer_project",
+            "gbla_layer_forward"} <= set(names)
     for n in names:
         assert hasattr(lib, n), n
 
@@ -161,3 +162,40 @@ def test_backward_workspace_and_validation(lib):
     for flags in (gbla.NO_GATE, gbla.NO_CONV, gbla.NO_NORM, gbla.BLA):
         assert _backward(lib, shape(flags=flags)) == 2
     assert _backward(lib, shape(flags=8)) == 1
+
+
+def lshape(**kw):
+    base = dict(batch=8, seqlen=2048, d_model=1024, heads=16, head_dim=64, conv_width=4,
+                max_seqlen=0, dtype=gbla.GBLA_BF16, eps=1e-6)
+    base.update(kw)
+    return gbla.LayerShape(**base)
+
+
+def test_layer_validation(lib):
+    s = lshape()
+    ws = lib.gbla_layer_workspace_bytes(ctypes.byref(s))
+    # four bf16 projections of every token and head, the gate logits and the core
+    assert ws >= 4 * 8 * 2048 * 16 * 64 * 2 + 8 * 2048 * 16 * 2
+    for bad in (lshape(dtype=gbla.GBLA_F32), lshape(d_model=100), lshape(d_model=0),
+                lshape(head_dim=48), lshape(conv_width=5), lshape(heads=0), lshape(seqlen=-1)):
+        assert lib.gbla_layer_workspace_bytes(ctypes.byref(bad)) == 0
+    P = ALIGNED
+    fwd = lambda s, **kw: lib.gbla_layer_forward(
+        ctypes.byref(s), kw.get("x", P), kw.get("c", P), kw.get("w", P), kw.get("g", P), None,
+        kw.get("ws", P), kw.get("wsb", ws), kw.get("out", P), None)
+    assert fwd(s, x=None) == 1
+    assert fwd(s, w=MIS) == 3
+    assert fwd(s, out=None) == 1
+    assert fwd(s, ws=None) == 4
+    assert fwd(s, ws=P + 64) == 3
+    assert fwd(s, wsb=1024) == 4
+    assert fwd(lshape(dtype=gbla.GBLA_F32)) == 2
+    assert fwd(lshape(d_model=96)) == 2
+    proj = lambda s, **kw: lib.gbla_layer_project(
+        ctypes.byref(s), kw.get("x", P), kw.get("c", P), kw.get("w", P), None, kw.get("q", P),
+        P, P, P, kw.get("a", P), None)
+    assert proj(s, q=None) == 1
+    assert proj(s, a=None) == 1
+    assert proj(s, a=P + 1) == 3
+    assert proj(s, x=MIS) == 3
+    assert proj(lshape(head_dim=16)) == 2
