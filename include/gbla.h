@@ -220,13 +220,16 @@ size_t gbla_layer_workspace_bytes(const gbla_layer_shape* shape);
  *   w_proj   [4*H*d + H, d_model] bf16: the output features' weight rows,
  *            W_Q's columns (h, e) at rows h*d + e, then W_K, W_V, W_R at
  *            offsets H*d, 2*H*d, 3*H*d, then w_g's H columns
+ *   workspace >= gbla_layer_workspace_bytes(shape) bytes (holds Xt)
  *   q, k, v, r  [B, H, L, d] or [H, T, d] bf16 outputs; a [B, H, L] or [H, T]
- * Base pointers 16-byte aligned (a: 2 bytes).  Does not synchronize.
+ * Base pointers 16-byte aligned (a: 2 bytes, workspace: 256).  Does not
+ * synchronize.
  */
 gbla_status gbla_layer_project(const gbla_layer_shape* shape, const void* x,
                                const float* conv_x, const void* w_proj,
-                               const int32_t* cu_seqlens, void* q, void* k, void* v,
-                               void* r, void* a, void* stream);
+                               const int32_t* cu_seqlens, void* workspace,
+                               size_t workspace_bytes, void* q, void* k, void* v, void* r,
+                               void* a, void* stream);
 
 /*
  * The whole layer: out [B, H, L, d] or [H, T, d] fp32 (the layout of

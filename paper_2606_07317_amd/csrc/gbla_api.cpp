@@ -150,6 +150,7 @@ gbla_status make_layer_plan(const gbla_layer_shape* s, bool ragged, LayerPlan* p
     off = align_up(off + bytes, 256);
     return at;
   };
+  L.off_xt = take((size_t)tokens * s->d_model * 2);
   L.off_q = take(act);
   L.off_k = take(act);
   L.off_v = take(act);
@@ -354,14 +355,19 @@ size_t gbla_layer_workspace_bytes(const gbla_layer_shape* shape) {
 }
 
 gbla_status gbla_layer_project(const gbla_layer_shape* shape, const void* x, const float* conv_x,
-                               const void* w_proj, const int32_t* cu_seqlens, void* q, void* k,
-                               void* v, void* r, void* a, void* stream) {
+                               const void* w_proj, const int32_t* cu_seqlens, void* workspace,
+                               size_t workspace_bytes, void* q, void* k, void* v, void* r,
+                               void* a, void* stream) {
   gbla::LayerPlan L;
   GBLA_TRY(gbla::make_layer_plan(shape, cu_seqlens != nullptr, &L));
   GBLA_TRY(check_used({x, conv_x, w_proj, q, k, v, r}));
   if (!a) return GBLA_ERR_INVALID_ARGUMENT;
   if (!gbla::aligned(a, 2)) return GBLA_ERR_MISALIGNED;
-  return gbla::launch_project(L, x, conv_x, w_proj, cu_seqlens, q, k, v, r, a,
+  if (!workspace) return GBLA_ERR_WORKSPACE;
+  if (!gbla::aligned(workspace, 256)) return GBLA_ERR_MISALIGNED;
+  if (workspace_bytes < L.total_bytes) return GBLA_ERR_WORKSPACE;
+  unsigned char* ws = static_cast<unsigned char*>(workspace);
+  return gbla::launch_project(L, x, conv_x, w_proj, cu_seqlens, ws + L.off_xt, q, k, v, r, a,
                               static_cast<hipStream_t>(stream));
 }
 
@@ -378,7 +384,7 @@ gbla_status gbla_layer_forward(const gbla_layer_shape* shape, const void* x, con
   unsigned char* ws = static_cast<unsigned char*>(workspace);
   hipStream_t st = static_cast<hipStream_t>(stream);
   void *q = ws + L.off_q, *k = ws + L.off_k, *v = ws + L.off_v, *r = ws + L.off_r, *a = ws + L.off_a;
-  GBLA_TRY(gbla::launch_project(L, x, conv_x, w_proj, cu_seqlens, q, k, v, r, a, st));
+  GBLA_TRY(gbla::launch_project(L, x, conv_x, w_proj, cu_seqlens, ws + L.off_xt, q, k, v, r, a, st));
   void* cws = ws + L.off_core;
   GBLA_TRY(gbla::launch_state(L.core, k, v, a, nullptr, cu_seqlens, cws, nullptr, nullptr,
                               nullptr, st));

@@ -106,12 +106,13 @@ struct LayerPlan {
   int32_t tokens;     // B * L or T
   int32_t features;   // 4 * H * d + H, the rows of the stacked projection weights
   Plan core;          // plan of the attention core (flags GBLA_NO_CONV)
-  size_t off_q, off_k, off_v, off_r, off_a, off_core, total_bytes;
+  size_t off_xt, off_q, off_k, off_v, off_r, off_a, off_core, total_bytes;
 };
 gbla_status make_layer_plan(const gbla_layer_shape* s, bool ragged, LayerPlan* p);
+// xt: tokens x d_model bf16 scratch for the convolved embeddings.
 gbla_status launch_project(const LayerPlan& p, const void* x, const float* conv_x,
-                           const void* w_proj, const int32_t* cu, void* q, void* k, void* v,
-                           void* r, void* a, hipStream_t stream);
+                           const void* w_proj, const int32_t* cu, void* xt, void* q, void* k,
+                           void* v, void* r, void* a, hipStream_t stream);
 
 // Streaming kernels (gbla_stream.hip): bf16 inputs, head dim 32 or 64.
 bool stream_supported(const Plan& p);

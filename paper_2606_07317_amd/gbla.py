@@ -81,7 +81,7 @@ def load_library(path: str = LIB_PATH):
     LP = ctypes.POINTER(LayerShape)
     lib.gbla_layer_workspace_bytes.argtypes = [LP]
     lib.gbla_layer_workspace_bytes.restype = sz
-    lib.gbla_layer_project.argtypes = [LP, P, P, P, P, P, P, P, P, P, P]
+    lib.gbla_layer_project.argtypes = [LP, P, P, P, P, P, sz, P, P, P, P, P, P]
     lib.gbla_layer_project.restype = ctypes.c_int
     lib.gbla_layer_forward.argtypes = [LP, P, P, P, P, P, P, sz, P, P]
     lib.gbla_layer_forward.restype = ctypes.c_int
@@ -335,11 +335,13 @@ def _check_layer(x, conv_x, w_proj, heads, head_dim, cu_seqlens):
 
 
 def layer_project(x, conv_x, w_proj, heads: int, head_dim: int, cu_seqlens=None,
-                  max_seqlen=None, stream=None) -> dict:
+                  max_seqlen=None, workspace=None, stream=None) -> dict:
     """Conv1D on x and the stacked projections: bf16 q, k, v, r in the
     attention layout ([B,H,L,d] or [H,T,d]) and the gate logits a."""
     _check_layer(x, conv_x, w_proj, heads, head_dim, cu_seqlens)
     shape = layer_shape(x, conv_x, heads, head_dim, 0.0, cu_seqlens, max_seqlen)
+    if workspace is None:
+        workspace = torch.empty(layer_workspace_bytes(shape), dtype=torch.uint8, device=x.device)
     if cu_seqlens is None:
         act = (shape.batch, heads, shape.seqlen, head_dim)
     else:
@@ -347,8 +349,9 @@ def layer_project(x, conv_x, w_proj, heads: int, head_dim: int, cu_seqlens=None,
     out = {n: torch.empty(act, dtype=torch.bfloat16, device=x.device) for n in ("q", "k", "v", "r")}
     out["a"] = torch.empty(act[:-1], dtype=torch.bfloat16, device=x.device)
     st = load_library().gbla_layer_project(
-        ctypes.byref(shape), _ptr(x), _ptr(conv_x), _ptr(w_proj), _ptr(cu_seqlens), _ptr(out["q"]),
-        _ptr(out["k"]), _ptr(out["v"]), _ptr(out["r"]), _ptr(out["a"]), _stream(stream))
+        ctypes.byref(shape), _ptr(x), _ptr(conv_x), _ptr(w_proj), _ptr(cu_seqlens), _ptr(workspace),
+        workspace.numel(), _ptr(out["q"]), _ptr(out["k"]), _ptr(out["v"]), _ptr(out["r"]),
+        _ptr(out["a"]), _stream(stream))
     _raise(st, "gbla_layer_project")
     return out
 

@@ -174,8 +174,8 @@ def lshape(**kw):
 def test_layer_validation(lib):
     s = lshape()
     ws = lib.gbla_layer_workspace_bytes(ctypes.byref(s))
-    # four bf16 projections of every token and head, the gate logits and the core
-    assert ws >= 4 * 8 * 2048 * 16 * 64 * 2 + 8 * 2048 * 16 * 2
+    # Xt, four bf16 projections of every token and head, the gate logits and the core
+    assert ws >= 8 * 2048 * 1024 * 2 + 4 * 8 * 2048 * 16 * 64 * 2 + 8 * 2048 * 16 * 2
     for bad in (lshape(dtype=gbla.GBLA_F32), lshape(d_model=100), lshape(d_model=0),
                 lshape(head_dim=48), lshape(conv_width=5), lshape(heads=0), lshape(seqlen=-1)):
         assert lib.gbla_layer_workspace_bytes(ctypes.byref(bad)) == 0
@@ -192,10 +192,12 @@ def test_layer_validation(lib):
     assert fwd(lshape(dtype=gbla.GBLA_F32)) == 2
     assert fwd(lshape(d_model=96)) == 2
     proj = lambda s, **kw: lib.gbla_layer_project(
-        ctypes.byref(s), kw.get("x", P), kw.get("c", P), kw.get("w", P), None, kw.get("q", P),
-        P, P, P, kw.get("a", P), None)
+        ctypes.byref(s), kw.get("x", P), kw.get("c", P), kw.get("w", P), None, kw.get("ws", P),
+        kw.get("wsb", ws), kw.get("q", P), P, P, P, kw.get("a", P), None)
     assert proj(s, q=None) == 1
     assert proj(s, a=None) == 1
     assert proj(s, a=P + 1) == 3
     assert proj(s, x=MIS) == 3
+    assert proj(s, ws=None) == 4
+    assert proj(s, wsb=1024) == 4
     assert proj(lshape(head_dim=16)) == 2
