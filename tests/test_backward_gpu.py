@@ -106,3 +106,17 @@ def test_backward_is_deterministic(G, dev):
     b = run_backward(G, inp, dy, dev)
     for n in NAMES:
         assert np.array_equal(a[n], b[n]), n
+
+
+@pytest.mark.parametrize("name", ["b8_n2048_d64", "b1_n32768_d64"])
+def test_backward_parity_full_size(G, dev, name):
+    """The benchmark workloads at full size, every element, in the launch
+    configuration bench.py --pass backward times."""
+    from oracle import gbla_backward
+    say("backward full size", name)
+    inp = inputs.make_inputs(name)
+    dy = inputs.make_cotangent(inp)
+    got = run_backward(G, inp, dy, dev)
+    ref = gbla_backward.backward_inputs(inp, dy)
+    for n in NAMES:
+        close_scaled(got[n], ref[n], TOL[inp.workload.dtype], n)
