@@ -293,14 +293,11 @@ bwd_query_kernel(Plan P, const T* __restrict__ qin, const T* __restrict__ rin,
         }
       }
       s1 = wave_sum(s1);
-      float dnum[CPL], s2 = 0.0f;
+      float dnum[CPL];
 #pragma unroll
-      for (int cc = 0; cc < CPL; ++cc) {
-        const float dov = rs * doh[cc] - rs * rs * rs / D * s1 * o[cc];
-        dnum[cc] = dov / den;
-        if (chan<D>(lane, cc) < D) s2 = fmaf(dov, o[cc], s2);
-      }
-      const float dden = -wave_sum(s2) / den;
+      for (int cc = 0; cc < CPL; ++cc) dnum[cc] = (rs * doh[cc] - rs * rs * rs / D * s1 * o[cc]) / den;
+      // do . o = eps rs^3 s1 exactly (rs^-2 = |o|^2/d + eps); see the matrix-core kernel
+      const float dden = -P.eps * rs * rs * rs * s1 / den;
 #pragma unroll
       for (int cc = 0; cc < CPL; ++cc) {
         const int e = chan<D>(lane, cc);
@@ -1123,16 +1120,15 @@ bwd_query_mfma_kernel(Plan P, const T* __restrict__ qin, const T* __restrict__ r
     }
     s1 = sum_groups(s1);
     const float c3 = rs * rs * rs / D * s1;
-    float dnum[NMB][4], s2 = 0.0f;
+    float dnum[NMB][4];
 #pragma unroll
     for (int kq = 0; kq < NMB; ++kq)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float dov = rs * doh[kq][i] - c3 * o[kq][i];
-        dnum[kq][i] = dov * inv_den;
-        s2 = fmaf(dov, o[kq][i], s2);
-      }
-    const float dden = -sum_groups(s2) * inv_den;
+      for (int i = 0; i < 4; ++i) dnum[kq][i] = (rs * doh[kq][i] - c3 * o[kq][i]) * inv_den;
+    // do . o = rs s1 (1 - rs^2 |o|^2 / d) = eps rs^3 s1 exactly (rs^-2 = |o|^2/d + eps):
+    // the RMSNorm leaves almost nothing along o, and summing do . o would
+    // return mostly the rounding of its terms.
+    const float dden = -P.eps * rs * rs * rs * s1 * inv_den;
     // dQh = S dnum + z dden
     f32x4_t acc2[NMB];
 #pragma unroll

@@ -102,3 +102,19 @@ def test_gate_gradient_has_no_centering_term(orc):
         full = gbla_backward.backward(*args, **meta)["da"]
         nocenter = mod.backward(*args, **meta)["da"]
         np.testing.assert_allclose(nocenter, full, rtol=1e-9, atol=1e-14)
+
+
+def test_rmsnorm_gradient_along_o_is_eps_sized():
+    """do = rs doh - rs^3/d (doh . o) o satisfies do . o = eps rs^3 (doh . o)
+    exactly (rs^-2 = mean(o^2) + eps): the kernels use this closed form for
+    dden = -(do . o) / den instead of summing do . o."""
+    rng = np.random.default_rng(5)
+    for eps in (0.0, 1e-6, 1e-3, 0.5):
+        o = rng.standard_normal((50, 16)) * rng.uniform(0.01, 10, (50, 1))
+        doh = rng.standard_normal((50, 16))
+        d = o.shape[1]
+        rs = 1.0 / np.sqrt(np.mean(o * o, axis=1) + eps)
+        s1 = np.sum(doh * o, axis=1)
+        do = rs[:, None] * doh - (rs ** 3 / d * s1)[:, None] * o
+        np.testing.assert_allclose(np.sum(do * o, axis=1), eps * rs ** 3 * s1,
+                                   rtol=1e-9, atol=1e-12 * np.abs(rs * s1).max())
