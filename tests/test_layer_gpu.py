@@ -99,3 +99,22 @@ def test_layer_forward_parity(G, dev, orc, name):
                                                  (err / (2e-2 * (1 + np.abs(ref)))).max() if err.size else 0))
     assert np.isfinite(got).all()
     assert (err <= 2e-2 * (1 + np.abs(ref))).all()
+
+
+def test_layer_forward_full_size_table5(G, dev, orc):
+    """The paper's Table 5 layer (batch 8, d_model 1024, 16 heads of 64) at
+    L = 2048, every output, in the launch configuration bench.py times."""
+    from oracle import gbla_layer
+    w = inputs.LAYER_WORKLOADS["layer_b8_n2048"]
+    say("layer forward full size", w.name)
+    inp = inputs.make_layer_inputs(w)
+    t = inputs.layer_device_tensors(inp, dev)
+    y = G.layer_forward(t["x"], t["conv_x"], t["w_proj"], t["gamma"], eps=w.eps)
+    torch.cuda.synchronize()
+    ref = gbla_layer.layer_forward(orc, inp.x, inp.conv_x, inp.w_proj, inp.gamma, eps=w.eps,
+                                   rounding=True, **oracle_meta(inp))["y"]
+    got = y.cpu().numpy().astype(np.float64)
+    err = np.abs(got - ref)
+    say("  y max abs %.3e, worst err/tol %.3f" % (err.max(), (err / (2e-2 * (1 + np.abs(ref)))).max()))
+    assert np.isfinite(got).all()
+    assert (err <= 2e-2 * (1 + np.abs(ref))).all()
