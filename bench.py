@@ -29,8 +29,9 @@ PROFILES = os.path.join(ROOT, "profiles")
 
 
 def kernel_source_hash() -> str:
+    """Hash of the sources the forward pass is built from (kernels and plan)."""
     h = hashlib.sha256()
-    for f in ("gbla_kernels.hip", "gbla_stream.hip", "gbla_device.h", "gbla_api.cpp", "gbla_plan.h"):
+    for f in ("gbla_kernels.hip", "gbla_stream.hip", "gbla_device.h", "gbla_plan.cpp", "gbla_plan.h"):
         with open(os.path.join(ROOT, "paper_2606_07317_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]

@@ -1,5 +1,6 @@
-// gbla_api.cpp -- the C ABI of libgbla.so: argument validation, the launch
-// plan and the entry points declared in include/gbla.h.
+// gbla_api.cpp -- the C ABI of libgbla.so: argument validation and the
+// entry points declared in include/gbla.h (the plans live in gbla_plan.cpp
+// and gbla_ext_plan.cpp).
 //
 // Every check runs on the host before anything is enqueued, and none of them
 // touches the HIP runtime, so a rejected call has no side effect.
@@ -7,185 +8,8 @@
 #include <stdint.h>
 
 #include "gbla.h"
+#include "gbla_ext.h"
 #include "gbla_plan.h"
-
-namespace gbla {
-namespace {
-
-constexpr int kMaxGridY = 65535;
-constexpr int64_t kMaxGridX = 2147483647LL;
-constexpr int kReadoutTile = 512;
-
-size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
-
-int64_t next_pow2(int64_t x) {
-  int64_t p = 1;
-  while (p < x) p <<= 1;
-  return p;
-}
-
-bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
-
-}  // namespace
-
-gbla_status make_plan(const gbla_shape* s, bool ragged, Plan* p) {
-  if (!s || !p) return GBLA_ERR_INVALID_ARGUMENT;
-  if (s->batch < 1 || s->heads < 1 || s->seqlen < 0) return GBLA_ERR_INVALID_ARGUMENT;
-  if (s->head_dim != 32 && s->head_dim != 64 && s->head_dim != 128) return GBLA_ERR_UNSUPPORTED;
-  if (s->conv_width < 1 || s->conv_width > 4) return GBLA_ERR_UNSUPPORTED;
-  if (s->dtype != GBLA_F32 && s->dtype != GBLA_BF16) return GBLA_ERR_UNSUPPORTED;
-  if (!(s->eps >= 0.0f) || !isfinite(s->eps)) return GBLA_ERR_INVALID_ARGUMENT;
-  if (ragged && s->max_seqlen < 0) return GBLA_ERR_INVALID_ARGUMENT;
-  if (s->heads > kMaxGridY) return GBLA_ERR_UNSUPPORTED;
-  if (s->flags & ~(uint32_t)GBLA_BLA) return GBLA_ERR_INVALID_ARGUMENT;
-
-  Plan q{};
-  q.nseq = s->batch;
-  q.heads = s->heads;
-  q.rows = s->seqlen;
-  q.d = s->head_dim;
-  q.W = s->conv_width;
-  q.dtype = s->dtype;
-  q.ragged = ragged ? 1 : 0;
-  q.eps = s->eps;
-  q.flags = s->flags;
-  q.tokens = ragged ? (int64_t)s->seqlen : (int64_t)s->batch * s->seqlen;
-
-  // Chunk of the state reduction: about one workgroup per CU over all heads,
-  // a power of two between 256 and 2048 tokens.  Depends on the shape only.
-  const int64_t work = q.tokens * q.heads;
-  int64_t chunk = next_pow2((work + 255) / 256);
-  if (chunk < 256) chunk = 256;
-  if (chunk > 2048) chunk = 2048;
-  q.chunk = (int32_t)chunk;
-  q.rtile = kReadoutTile;
-
-  // Upper bounds valid for both layouts: sum_s max(1, ceil(len_s / u)) <=
-  // tokens / u + N.  The partial records are sized with this bound so the
-  // workspace layout is the same for the dense and the ragged call.
-  const int64_t units_cap = q.tokens / q.chunk + q.nseq;
-  const int64_t runits_cap = q.tokens / q.rtile + q.nseq;
-  if (units_cap > kMaxGridX || runits_cap > kMaxGridX) return GBLA_ERR_UNSUPPORTED;
-  if (ragged) {
-    q.chunks_per_seq = 0;
-    q.rtiles_per_seq = 0;
-    q.units = (int32_t)units_cap;
-    q.runits = (int32_t)runits_cap;
-  } else {
-    int64_t cps = ((int64_t)q.rows + q.chunk - 1) / q.chunk;
-    int64_t rps = ((int64_t)q.rows + q.rtile - 1) / q.rtile;
-    if (cps < 1) cps = 1;
-    if (rps < 1) rps = 1;
-    q.chunks_per_seq = (int32_t)cps;
-    q.rtiles_per_seq = (int32_t)rps;
-    q.units = (int32_t)(cps * q.nseq);
-    q.runits = (int32_t)(rps * q.nseq);
-  }
-
-  q.rec_floats = (int32_t)align_up((size_t)q.d * q.d + q.d + 2, 64);
-  const size_t nmb = q.d / 16 + 1, nkb = q.d / 32;
-  const size_t lane_bytes = q.dtype == GBLA_BF16 ? 16 : 32;
-  q.frag_bytes = align_up(nmb * nkb * 64 * lane_bytes, 256);
-  q.off_partials = 0;
-  const size_t part_bytes = (size_t)units_cap * q.heads * q.rec_floats * sizeof(float);
-  q.off_frags = align_up(q.off_partials + part_bytes, 256);
-  q.total_bytes = align_up(q.off_frags + (size_t)q.nseq * q.heads * q.frag_bytes, 256);
-  *p = q;
-  return GBLA_OK;
-}
-
-Plan backward_plan(const Plan& p) {
-  // Units of 512 tokens, whatever the forward's: long enough to amortise each
-  // workgroup's set-up (A operands, the ordered wave sums), short enough for
-  // two workgroups per CU at n = 32768, H = 8 (measured against 256 and 1024).
-  Plan b = p;
-  b.chunk = 512;
-  if (p.ragged) {
-    b.units = (int32_t)(b.tokens / b.chunk + b.nseq);
-  } else {
-    int64_t cps = ((int64_t)b.rows + b.chunk - 1) / b.chunk;
-    if (cps < 1) cps = 1;
-    b.chunks_per_seq = (int32_t)cps;
-    b.units = (int32_t)(cps * b.nseq);
-  }
-  return b;
-}
-
-gbla_status make_layer_plan(const gbla_layer_shape* s, bool ragged, LayerPlan* p) {
-  if (!s || !p) return GBLA_ERR_INVALID_ARGUMENT;
-  if (s->batch < 1 || s->heads < 1 || s->seqlen < 0) return GBLA_ERR_INVALID_ARGUMENT;
-  if (s->dtype != GBLA_BF16) return GBLA_ERR_UNSUPPORTED;
-  if (s->d_model < 64 || s->d_model > 16384 || s->d_model % 64 != 0) return GBLA_ERR_UNSUPPORTED;
-  if (s->conv_width < 1 || s->conv_width > 4) return GBLA_ERR_UNSUPPORTED;
-  LayerPlan L{};
-  L.nseq = s->batch;
-  L.rows = s->seqlen;
-  L.d_model = s->d_model;
-  L.heads = s->heads;
-  L.d = s->head_dim;
-  L.W = s->conv_width;
-  L.ragged = ragged ? 1 : 0;
-  const int64_t tokens = ragged ? (int64_t)s->seqlen : (int64_t)s->batch * s->seqlen;
-  const int64_t features = (int64_t)s->heads * (4 * (int64_t)s->head_dim + 1);
-  // 32-bit buffer offsets over X and the weights
-  if (tokens * s->d_model * 2 >= (int64_t(1) << 31)) return GBLA_ERR_UNSUPPORTED;
-  if (features * s->d_model * 2 >= (int64_t(1) << 31)) return GBLA_ERR_UNSUPPORTED;
-  L.tokens = (int32_t)tokens;
-  L.features = (int32_t)features;
-  gbla_shape cs{};
-  cs.batch = s->batch;
-  cs.heads = s->heads;
-  cs.seqlen = s->seqlen;
-  cs.head_dim = s->head_dim;
-  cs.conv_width = 1;
-  cs.max_seqlen = ragged ? s->max_seqlen : 0;
-  cs.dtype = GBLA_BF16;
-  cs.eps = s->eps;
-  cs.flags = GBLA_NO_CONV;
-  gbla_status st = make_plan(&cs, ragged, &L.core);
-  if (st != GBLA_OK) return st;
-  const size_t act = (size_t)tokens * s->heads * s->head_dim * 2;
-  size_t off = 0;
-  auto take = [&](size_t bytes) {
-    const size_t at = off;
-    off = align_up(off + bytes, 256);
-    return at;
-  };
-  L.off_xt = take((size_t)tokens * s->d_model * 2);
-  L.off_q = take(act);
-  L.off_k = take(act);
-  L.off_v = take(act);
-  L.off_r = take(act);
-  L.off_a = take((size_t)tokens * s->heads * 2);
-  L.off_core = take(L.core.total_bytes);
-  L.total_bytes = off;
-  *p = L;
-  return GBLA_OK;
-}
-
-BwdLayout make_bwd_layout(const Plan& p) {
-  BwdLayout L{};
-  const size_t pairs = (size_t)p.nseq * p.heads, d = p.d, f = sizeof(float);
-  const size_t unit_recs = (size_t)p.units * p.heads;
-  size_t off = 0;
-  auto take = [&](size_t bytes) {
-    const size_t at = off;
-    off = align_up(off + bytes, 256);
-    return at;
-  };
-  L.off_S = take(pairs * d * d * f);
-  L.off_z = take(pairs * d * f);
-  L.off_mz = take(pairs * 2 * f);
-  L.off_dsp = take(unit_recs * p.rec_floats * f);
-  L.off_dS = take(pairs * (d * d + d) * f);
-  L.off_dgp = take(unit_recs * d * f);
-  L.off_dxt = take(3 * (size_t)p.tokens * p.heads * d * f);
-  L.off_dcp = take(unit_recs * 3 * d * 4 * f);
-  L.total_bytes = off;
-  return L;
-}
-
-}  // namespace gbla
 
 using gbla::Plan;
 

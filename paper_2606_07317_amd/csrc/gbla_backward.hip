@@ -26,6 +26,7 @@
 #include <stdint.h>
 
 #include "gbla_device.h"
+#include "gbla_ext.h"
 #include "gbla_plan.h"
 
 namespace gbla {

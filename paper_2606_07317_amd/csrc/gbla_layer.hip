@@ -19,6 +19,7 @@
 #include <stdint.h>
 
 #include "gbla_device.h"
+#include "gbla_ext.h"
 #include "gbla_plan.h"
 
 namespace gbla {
