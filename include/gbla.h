@@ -176,8 +176,9 @@ size_t gbla_backward_workspace_bytes(const gbla_shape* shape);
  *   d_conv_w         [3,H,d,W] fp32, summed over the batch
  *   d_norm_w         [H,d]     fp32, summed over the batch
  * Every output is overwritten (not accumulated).  Reductions run in an order
- * fixed by the shape: repeated calls give the same bits.  Only the full layer
- * (shape->flags == 0) is built: other flags return GBLA_ERR_UNSUPPORTED.
+ * fixed by the shape: repeated calls give the same bits.  Under the ablation
+ * switches (GBLA_NO_*) the inputs a switch removes, and their gradients, may
+ * be NULL and are neither read nor written.
  */
 gbla_status gbla_backward(const gbla_shape* shape, const void* q, const void* k,
                           const void* v, const void* gate_logits, const void* out_gate,

@@ -87,9 +87,11 @@ def _conv_backward(x, dxt, w):
     return dx, dw
 
 
-def _one(q, k, v, a, r, cw, gamma, dy, eps):
+def _one(q, k, v, a, r, cw, gamma, dy, eps, norm=True):
     """Backward of one (sequence, head): returns the input gradients and this
-    slice's contributions to dconv_w [3, d, W] and dgamma [d]."""
+    slice's contributions to dconv_w [3, d, W] and dgamma [d].  norm=False is
+    the layer without the gated RMSNorm (y = o): step 1 and 2 drop out and
+    do = dy."""
     L, d = q.shape
     if L == 0:
         z0 = np.zeros((0, d))
@@ -105,14 +107,19 @@ def _one(q, k, v, a, r, cw, gamma, dy, eps):
     o = num / den[:, None]
     rs = 1.0 / np.sqrt(np.mean(o * o, axis=1) + eps)
     oh = o * rs[:, None]
-    sig = 1.0 / (1.0 + np.exp(-r))
-    silu = r * sig
-    # 1. gated norm
-    doh = dy * gamma * silu
-    dgamma = np.sum(dy * oh * silu, axis=0)
-    dr = dy * oh * gamma * sig * (1.0 + r * (1.0 - sig))
-    # 2. RMSNorm
-    do = rs[:, None] * doh - (rs ** 3 / d * np.sum(doh * o, axis=1))[:, None] * o
+    if norm:
+        sig = 1.0 / (1.0 + np.exp(-r))
+        silu = r * sig
+        # 1. gated norm
+        doh = dy * gamma * silu
+        dgamma = np.sum(dy * oh * silu, axis=0)
+        dr = dy * oh * gamma * sig * (1.0 + r * (1.0 - sig))
+        # 2. RMSNorm
+        do = rs[:, None] * doh - (rs ** 3 / d * np.sum(doh * o, axis=1))[:, None] * o
+    else:
+        dgamma = np.zeros(d)
+        dr = np.zeros_like(r)
+        do = dy
     # 3. division
     dnum = do / den[:, None]
     dden = -np.sum(do * o, axis=1) / den
@@ -138,12 +145,13 @@ def _one(q, k, v, a, r, cw, gamma, dy, eps):
 
 
 def backward(q, k, v, a, r, conv_w, gamma, dy, *, nseq: int, heads: int, rows: int, d: int,
-             W: int, dtype: str, eps: float, cu_seqlens: Optional[np.ndarray] = None) -> dict:
+             W: int, dtype: str, eps: float, cu_seqlens: Optional[np.ndarray] = None,
+             norm: bool = True) -> dict:
     """Gradients of sum(y * dy) with respect to every input of the forward
     pass.  Layouts as in the forward oracle: dense [nseq, H, rows, d] or
     ragged [H, T, d] with ``cu_seqlens``; logits without the trailing d.
     Returns fp64 dq, dk, dv, da, dr (input layouts), dconv_w [3, H, d, W] and
-    dgamma [H, d]."""
+    dgamma [H, d].  norm=False: y = o (dr and dgamma are zero)."""
     acts = [_widen(x, dtype) for x in (q, k, v, a, r)]
     dyv = np.asarray(dy, dtype=np.float64)
     cw = np.asarray(conv_w, dtype=np.float64).reshape(3, heads, d, W)
@@ -167,7 +175,7 @@ def backward(q, k, v, a, r, conv_w, gamma, dy, *, nseq: int, heads: int, rows: i
                 sl = (s, h)
             else:
                 sl = (h, slice(int(cu_seqlens[s]), int(cu_seqlens[s + 1])))
-            res = _one(qa[sl], ka[sl], va[sl], aa[sl], ra[sl], cw[:, h], gm[h], dyv[sl], eps)
+            res = _one(qa[sl], ka[sl], va[sl], aa[sl], ra[sl], cw[:, h], gm[h], dyv[sl], eps, norm)
             for name, val in zip(("dq", "dk", "dv", "da", "dr"), res[:5]):
                 out[name][sl] = val
             out["dconv_w"][:, h] += res[5]
@@ -175,12 +183,26 @@ def backward(q, k, v, a, r, conv_w, gamma, dy, *, nseq: int, heads: int, rows: i
     return out
 
 
-def backward_inputs(inp, dy) -> dict:
+def backward_inputs(inp, dy, gate: bool = True, conv: bool = True, norm: bool = True) -> dict:
     """``backward`` on a ``paper_2606_07317_amd.inputs.Inputs`` batch and its
-    cotangent ``dy``."""
+    cotangent ``dy``.  The ablation switches (Section 4, "Ablation") go
+    through the inputs as in the forward oracle: gate=False is constant
+    logits (uniform gates), conv=False identity taps, norm=False y = o.  The
+    gradients of a removed input are returned as zeros."""
     w = inp.workload
     ragged = inp.cu_seqlens is not None
-    return backward(inp.q, inp.k, inp.v, inp.a, inp.r, inp.conv_w, inp.gamma, dy,
-                    nseq=inp.nseq, heads=w.heads, rows=inp.rows if ragged else w.seqlen,
-                    d=w.head_dim, W=w.conv_width, dtype=w.dtype, eps=inp.eps,
-                    cu_seqlens=inp.cu_seqlens)
+    a, cw = inp.a, inp.conv_w
+    if not gate:
+        a = np.zeros_like(inp.a)  # +0.0 in either storage (bf16 bit patterns or fp32)
+    if not conv:
+        cw = np.zeros(inp.conv_w.shape)
+        cw[..., w.conv_width - 1] = 1.0
+    g = backward(inp.q, inp.k, inp.v, a, inp.r, cw, inp.gamma, dy,
+                 nseq=inp.nseq, heads=w.heads, rows=inp.rows if ragged else w.seqlen,
+                 d=w.head_dim, W=w.conv_width, dtype=w.dtype,
+                 eps=inp.eps, cu_seqlens=inp.cu_seqlens, norm=norm)
+    if not gate:
+        g["da"] = np.zeros_like(g["da"])
+    if not conv:
+        g["dconv_w"] = np.zeros_like(g["dconv_w"])
+    return g

@@ -156,13 +156,24 @@ gbla_status gbla_backward(const gbla_shape* shape, const void* q, const void* k,
                           float* d_norm_w, void* stream) {
   Plan p0;
   GBLA_TRY(gbla::make_plan(shape, cu_seqlens != nullptr, &p0));
-  if (p0.flags != 0) return GBLA_ERR_UNSUPPORTED;
   const Plan p = gbla::backward_plan(p0);
-  GBLA_TRY(check_acts(p, {q, k, v, out_gate, dy, dq, dk, dv, d_out_gate}));
-  GBLA_TRY(check_used({conv_w, norm_w, d_conv_w, d_norm_w}));
-  GBLA_TRY(check_logits(p, gate_logits));
-  if (!d_gate_logits) return GBLA_ERR_INVALID_ARGUMENT;
-  if (!gbla::aligned(d_gate_logits, sizeof(float))) return GBLA_ERR_MISALIGNED;
+  // inputs a switch removes, and their gradients, are NULL inside the library
+  gate_logits = unless(p, GBLA_NO_GATE, gate_logits);
+  d_gate_logits = unless(p, GBLA_NO_GATE, d_gate_logits);
+  conv_w = unless(p, GBLA_NO_CONV, conv_w);
+  d_conv_w = unless(p, GBLA_NO_CONV, d_conv_w);
+  out_gate = unless(p, GBLA_NO_NORM, out_gate);
+  norm_w = unless(p, GBLA_NO_NORM, norm_w);
+  d_out_gate = unless(p, GBLA_NO_NORM, d_out_gate);
+  d_norm_w = unless(p, GBLA_NO_NORM, d_norm_w);
+  GBLA_TRY(check_acts(p, {q, k, v, dy, dq, dk, dv}));
+  if (!(p.flags & GBLA_NO_CONV)) GBLA_TRY(check_used({conv_w, d_conv_w}));
+  if (!(p.flags & GBLA_NO_NORM)) GBLA_TRY(check_used({out_gate, norm_w, d_out_gate, d_norm_w}));
+  if (!(p.flags & GBLA_NO_GATE)) {
+    GBLA_TRY(check_logits(p, gate_logits));
+    if (!d_gate_logits) return GBLA_ERR_INVALID_ARGUMENT;
+    if (!gbla::aligned(d_gate_logits, sizeof(float))) return GBLA_ERR_MISALIGNED;
+  }
   const gbla::BwdLayout L = gbla::make_bwd_layout(p);
   if (!workspace) return GBLA_ERR_WORKSPACE;
   if (!gbla::aligned(workspace, 256)) return GBLA_ERR_MISALIGNED;

@@ -51,6 +51,11 @@ __device__ __forceinline__ void wave_lds_sync() {
 }
 
 __device__ __forceinline__ float phi_f(float u) { return u > 0.0f ? u + 1.0f : expf(u); }
+
+// Gate logit i, or 0 without gate logits (the no-key-gating switch: uniform
+// gates, the softmax of constant logits).
+template <typename T>
+__device__ __forceinline__ float logit(const T* a, int64_t i) { return a ? act<T>(a, i) : 0.0f; }
 // Hardware-exp forms for the matrix-core kernels (a few ulp; the gradients
 // are held to fp32-sum accuracy, far above that).
 __device__ __forceinline__ float phi_fast(float u) { return u > 0.0f ? u + 1.0f : __expf(u); }
@@ -103,7 +108,7 @@ bwd_state_kernel(Plan P, const T* __restrict__ kin, const T* __restrict__ vin,
   const int64_t t1 = min(len, t0 + (int64_t)P.chunk);
 
   float ml = -INFINITY;
-  for (int64_t j = t0 + tid; j < t1; j += kThreads) ml = fmaxf(ml, act<T>(ain, base_row + j));
+  for (int64_t j = t0 + tid; j < t1; j += kThreads) ml = fmaxf(ml, logit<T>(ain, base_row + j));
   const float m = block_max(ml, red);
 
   float wk[CPL][4], wv[CPL][4];
@@ -124,7 +129,7 @@ bwd_state_kernel(Plan P, const T* __restrict__ kin, const T* __restrict__ vin,
       const int slot = wave * C::kTok + k;
       const int64_t j = b0 + slot;
       const bool live = j < t1;  // wave-uniform
-      const float w = live ? expf(act<T>(ain, base_row + j) - m) : 0.0f;
+      const float w = live ? expf(logit<T>(ain, base_row + j) - m) : 0.0f;
       if (lane == 0) l_acc += w;
 #pragma unroll
       for (int cc = 0; cc < CPL; ++cc) {
@@ -179,7 +184,7 @@ bwd_state_kernel(Plan P, const T* __restrict__ kin, const T* __restrict__ vin,
 // ---------------------------------------------------------------------------
 // Query pass: grid (units, H).
 // ---------------------------------------------------------------------------
-template <typename T, int D>
+template <typename T, int D, bool kNorm>
 __global__ void __launch_bounds__(kThreads)
 bwd_query_kernel(Plan P, const T* __restrict__ qin, const T* __restrict__ rin,
                  const float* __restrict__ dy, const float* __restrict__ conv_w,
@@ -213,7 +218,7 @@ bwd_query_kernel(Plan P, const T* __restrict__ qin, const T* __restrict__ rin,
   for (int cc = 0; cc < CPL; ++cc) {
     const int e = min(chan<D>(lane, cc), D - 1);
     load_taps4(conv_w, P.heads, h, 0, D, P.W, e, wq[cc]);
-    gm[cc] = gamma[(size_t)h * D + e];
+    gm[cc] = kNorm ? gamma[(size_t)h * D + e] : 1.0f;
     dg_acc[cc] = 0.0f;
   }
   const int ds_e = tid % D, ds_c0 = tid / D;
@@ -277,28 +282,40 @@ bwd_query_kernel(Plan P, const T* __restrict__ qin, const T* __restrict__ rin,
         o[cc] = num[cc] / den;
         if (chan<D>(lane, cc) < D) ss = fmaf(o[cc], o[cc], ss);
       }
-      const float rs = 1.0f / sqrtf(wave_sum(ss) / D + P.eps);
-      float doh[CPL], s1 = 0.0f;
+      float dnum[CPL], dden;
+      if constexpr (kNorm) {
+        const float rs = 1.0f / sqrtf(wave_sum(ss) / D + P.eps);
+        float doh[CPL], s1 = 0.0f;
 #pragma unroll
-      for (int cc = 0; cc < CPL; ++cc) {
-        const int e = chan<D>(lane, cc);
-        doh[cc] = 0.0f;
-        if (e < D) {
-          const float rv = act<T>(rin, row * D + e), dyv = dy[row * D + e];
-          const float sig = 1.0f / (1.0f + expf(-rv)), silu = rv * sig;
-          const float oh = o[cc] * rs;
-          doh[cc] = dyv * gm[cc] * silu;
-          dg_acc[cc] = fmaf(dyv * oh, silu, dg_acc[cc]);
-          dr[row * D + e] = dyv * oh * gm[cc] * sig * (1.0f + rv * (1.0f - sig));
-          s1 = fmaf(doh[cc], o[cc], s1);
+        for (int cc = 0; cc < CPL; ++cc) {
+          const int e = chan<D>(lane, cc);
+          doh[cc] = 0.0f;
+          if (e < D) {
+            const float rv = act<T>(rin, row * D + e), dyv = dy[row * D + e];
+            const float sig = 1.0f / (1.0f + expf(-rv)), silu = rv * sig;
+            const float oh = o[cc] * rs;
+            doh[cc] = dyv * gm[cc] * silu;
+            dg_acc[cc] = fmaf(dyv * oh, silu, dg_acc[cc]);
+            dr[row * D + e] = dyv * oh * gm[cc] * sig * (1.0f + rv * (1.0f - sig));
+            s1 = fmaf(doh[cc], o[cc], s1);
+          }
         }
-      }
-      s1 = wave_sum(s1);
-      float dnum[CPL];
+        s1 = wave_sum(s1);
 #pragma unroll
-      for (int cc = 0; cc < CPL; ++cc) dnum[cc] = (rs * doh[cc] - rs * rs * rs / D * s1 * o[cc]) / den;
-      // do . o = eps rs^3 s1 exactly (rs^-2 = |o|^2/d + eps); see the matrix-core kernel
-      const float dden = -P.eps * rs * rs * rs * s1 / den;
+        for (int cc = 0; cc < CPL; ++cc) dnum[cc] = (rs * doh[cc] - rs * rs * rs / D * s1 * o[cc]) / den;
+        // do . o = eps rs^3 s1 exactly (rs^-2 = |o|^2/d + eps); see the matrix-core kernel
+        dden = -P.eps * rs * rs * rs * s1 / den;
+      } else {  // y = o: do = dy
+        float s2 = 0.0f;
+#pragma unroll
+        for (int cc = 0; cc < CPL; ++cc) {
+          const int e = chan<D>(lane, cc);
+          const float dyv = e < D ? dy[row * D + e] : 0.0f;
+          dnum[cc] = dyv / den;
+          s2 = fmaf(dyv, o[cc], s2);
+        }
+        dden = -wave_sum(s2) / den;
+      }
 #pragma unroll
       for (int cc = 0; cc < CPL; ++cc) {
         const int e = chan<D>(lane, cc);
@@ -468,7 +485,7 @@ bwd_key_kernel(Plan P, const T* __restrict__ kin, const T* __restrict__ vin,
       }
     }
     const float dg = wave_sum(dgl);
-    if (lane == 0) da[row] = gj * dg;
+    if (da && lane == 0) da[row] = gj * dg;
     // dvt[e] = g sum_c dS[c][e] P[c]
 #pragma unroll
     for (int cc = 0; cc < CPL; ++cc) {
@@ -587,7 +604,7 @@ bwd_param_kernel(Plan P, const int32_t* __restrict__ cu, const float* __restrict
   if (tid < 64 && live) {
     const float sum = (red[0][tid] + red[1][tid]) + (red[2][tid] + red[3][tid]);
     if (e < D) {
-      dgamma[(size_t)h * D + e] = sum;
+      if (dgamma) dgamma[(size_t)h * D + e] = sum;
     } else {
       const int x = e - D, tensor = x / (D * P.W), rem = x % (D * P.W);
       dconv[((size_t)tensor * P.heads + h) * D * P.W + rem] = sum;
@@ -915,13 +932,15 @@ bwd_state_mfma_kernel(Plan P, const T* __restrict__ kin, const T* __restrict__ v
     tv[tid] = (f32x4_t){w4[0], w4[1], w4[2], w4[3]};
   }
   float ml = -INFINITY;
-  for (int j = t0 + tid; j < t1; j += kThreads) ml = fmaxf(ml, act<T>(ain, base_row + j));
+  for (int j = t0 + tid; j < t1; j += kThreads) ml = fmaxf(ml, logit<T>(ain, base_row + j));
   const float m = block_max(ml, red4);  // its barriers also publish tk, tv
 
   const uint32_t rows = (uint32_t)len * D;
   const __amdgpu_buffer_rsrc_t rk = make_rsrc(kin + base_row * D, rows * sizeof(T));
   const __amdgpu_buffer_rsrc_t rv = make_rsrc(vin + base_row * D, rows * sizeof(T));
-  const __amdgpu_buffer_rsrc_t ra = make_rsrc(ain + base_row, (uint32_t)len * sizeof(T));
+  // no gate logits: an empty range, so every logit reads as 0
+  const __amdgpu_buffer_rsrc_t ra =
+      ain ? make_rsrc(ain + base_row, (uint32_t)len * sizeof(T)) : make_rsrc(kin, 0u);
   f32x4_t acc[C::kBlocks];
 #pragma unroll
   for (int k = 0; k < C::kBlocks; ++k) acc[k] = (f32x4_t){0.0f, 0.0f, 0.0f, 0.0f};
@@ -983,7 +1002,7 @@ bwd_state_mfma_kernel(Plan P, const T* __restrict__ kin, const T* __restrict__ v
 // ---------------------------------------------------------------------------
 // Query pass, matrix-core version.
 // ---------------------------------------------------------------------------
-template <typename T, int D>
+template <typename T, int D, bool kNorm>
 __global__ void __launch_bounds__(kThreads, 2)
 bwd_query_mfma_kernel(Plan P, const T* __restrict__ qin, const T* __restrict__ rin,
                       const float* __restrict__ dy, const float* __restrict__ conv_w,
@@ -1018,7 +1037,7 @@ bwd_query_mfma_kernel(Plan P, const T* __restrict__ qin, const T* __restrict__ r
     load_taps4(conv_w, P.heads, h, 0, D, P.W, tid, w4);
     tq[tid] = (f32x4_t){w4[0], w4[1], w4[2], w4[3]};
     zs[tid] = z[tid];
-    gs[tid] = gamma[(size_t)h * D + tid];
+    gs[tid] = kNorm ? gamma[(size_t)h * D + tid] : 1.0f;
   }
   float dzacc[NMB][4], dgacc[NMB][4];
 #pragma unroll
@@ -1037,10 +1056,13 @@ bwd_query_mfma_kernel(Plan P, const T* __restrict__ qin, const T* __restrict__ r
 
   const uint32_t rows = (uint32_t)len * D;
   const __amdgpu_buffer_rsrc_t rq = make_rsrc(qin + base_row * D, rows * sizeof(T));
-  const __amdgpu_buffer_rsrc_t rr = make_rsrc(rin + base_row * D, rows * sizeof(T));
+  // without the gated norm r is not read (an empty range) and dr not written
+  const __amdgpu_buffer_rsrc_t rr =
+      kNorm ? make_rsrc(rin + base_row * D, rows * sizeof(T)) : make_rsrc(qin, 0u);
   const __amdgpu_buffer_rsrc_t rdy = make_rsrc(dy + base_row * D, rows * 4u);
   const __amdgpu_buffer_rsrc_t rdq = make_rsrc(dqt + base_row * D, rows * 4u);
-  const __amdgpu_buffer_rsrc_t rdr = make_rsrc(dr + base_row * D, rows * 4u);
+  const __amdgpu_buffer_rsrc_t rdr =
+      kNorm ? make_rsrc(dr + base_row * D, rows * 4u) : make_rsrc(dqt, 0u);
   float* X = stg[wave][0];
   float* Y = stg[wave][1];
   __syncthreads();  // fragments built; the staging area is free again
@@ -1100,36 +1122,48 @@ bwd_query_mfma_kernel(Plan P, const T* __restrict__ qin, const T* __restrict__ r
         o[kq][i] = acc1[kq][i] * inv_den;
         ss = fmaf(o[kq][i], o[kq][i], ss);
       }
-    const float rs = 1.0f / sqrtf(sum_groups(ss) / D + P.eps);
-    // gated RMSNorm backward
-    float doh[NMB][4], s1 = 0.0f;
+    float dnum[NMB][4], dden;
+    if constexpr (kNorm) {
+      const float rs = 1.0f / sqrtf(sum_groups(ss) / D + P.eps);
+      // gated RMSNorm backward
+      float doh[NMB][4], s1 = 0.0f;
 #pragma unroll
-    for (int kq = 0; kq < NMB; ++kq) {
-      const f32x4_t gm = *reinterpret_cast<const f32x4_t*>(&gs[16 * kq + 4 * g]);
-      float drv[4];
+      for (int kq = 0; kq < NMB; ++kq) {
+        const f32x4_t gm = *reinterpret_cast<const f32x4_t*>(&gs[16 * kq + 4 * g]);
+        float drv[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float r = rv[kq][i], d = dyv[kq][i];
-        const float sig = sigmoid_fast(r), silu = r * sig;
-        const float oh = o[kq][i] * rs;
-        doh[kq][i] = d * gm[i] * silu;
-        dgacc[kq][i] = fmaf(d * oh, silu, dgacc[kq][i]);
-        drv[i] = d * oh * gm[i] * sig * (1.0f + r * (1.0f - sig));
-        s1 = fmaf(doh[kq][i], o[kq][i], s1);
+        for (int i = 0; i < 4; ++i) {
+          const float r = rv[kq][i], d = dyv[kq][i];
+          const float sig = sigmoid_fast(r), silu = r * sig;
+          const float oh = o[kq][i] * rs;
+          doh[kq][i] = d * gm[i] * silu;
+          dgacc[kq][i] = fmaf(d * oh, silu, dgacc[kq][i]);
+          drv[i] = d * oh * gm[i] * sig * (1.0f + r * (1.0f - sig));
+          s1 = fmaf(doh[kq][i], o[kq][i], s1);
+        }
+        store4(rdr, eoff<D>(cur, 16 * kq + 4 * g), drv);
       }
-      store4(rdr, eoff<D>(cur, 16 * kq + 4 * g), drv);
+      s1 = sum_groups(s1);
+      const float c3 = rs * rs * rs / D * s1;
+#pragma unroll
+      for (int kq = 0; kq < NMB; ++kq)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) dnum[kq][i] = (rs * doh[kq][i] - c3 * o[kq][i]) * inv_den;
+      // do . o = rs s1 (1 - rs^2 |o|^2 / d) = eps rs^3 s1 exactly (rs^-2 = |o|^2/d + eps):
+      // the RMSNorm leaves almost nothing along o, and summing do . o would
+      // return mostly the rounding of its terms.
+      dden = -P.eps * rs * rs * rs * s1 * inv_den;
+    } else {  // y = o: do = dy
+      float s2 = 0.0f;
+#pragma unroll
+      for (int kq = 0; kq < NMB; ++kq)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          dnum[kq][i] = dyv[kq][i] * inv_den;
+          s2 = fmaf(dyv[kq][i], o[kq][i], s2);
+        }
+      dden = -sum_groups(s2) * inv_den;
     }
-    s1 = sum_groups(s1);
-    const float c3 = rs * rs * rs / D * s1;
-    float dnum[NMB][4];
-#pragma unroll
-    for (int kq = 0; kq < NMB; ++kq)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) dnum[kq][i] = (rs * doh[kq][i] - c3 * o[kq][i]) * inv_den;
-    // do . o = rs s1 (1 - rs^2 |o|^2 / d) = eps rs^3 s1 exactly (rs^-2 = |o|^2/d + eps):
-    // the RMSNorm leaves almost nothing along o, and summing do . o would
-    // return mostly the rounding of its terms.
-    const float dden = -P.eps * rs * rs * rs * s1 * inv_den;
     // dQh = S dnum + z dden
     f32x4_t acc2[NMB];
 #pragma unroll
@@ -1210,10 +1244,13 @@ bwd_key_mfma_kernel(Plan P, const T* __restrict__ kin, const T* __restrict__ vin
   const uint32_t rows = (uint32_t)len * D;
   const __amdgpu_buffer_rsrc_t rk = make_rsrc(kin + base_row * D, rows * sizeof(T));
   const __amdgpu_buffer_rsrc_t rv = make_rsrc(vin + base_row * D, rows * sizeof(T));
-  const __amdgpu_buffer_rsrc_t ra = make_rsrc(ain + base_row, (uint32_t)len * sizeof(T));
+  // absent gate logits read as 0 and an absent da is not written (empty ranges)
+  const __amdgpu_buffer_rsrc_t ra =
+      ain ? make_rsrc(ain + base_row, (uint32_t)len * sizeof(T)) : make_rsrc(kin, 0u);
   const __amdgpu_buffer_rsrc_t rdk = make_rsrc(dkt + base_row * D, rows * 4u);
   const __amdgpu_buffer_rsrc_t rdv = make_rsrc(dvt + base_row * D, rows * 4u);
-  const __amdgpu_buffer_rsrc_t rda = make_rsrc(da + base_row, (uint32_t)t1 * 4u);
+  const __amdgpu_buffer_rsrc_t rda =
+      da ? make_rsrc(da + base_row, (uint32_t)t1 * 4u) : make_rsrc(dkt, 0u);
 
   // the wave's contiguous quarter of the unit, 16 tokens at a time
   const int q4 = P.chunk / 4, w0 = t0 + wave * q4, w1 = min(t1, w0 + q4);
@@ -1380,9 +1417,14 @@ gbla_status run_backward(const Plan& p, const BwdLayout& L, const void* q, const
                          (const T*)k, (const T*)v, (const T*)a, conv_w, cu, dsp);
       gbla_status e = launch_combine_f32(p, cu, dsp, S, z, mz, st);
       if (e != GBLA_OK) return e;
-      hipLaunchKernelGGL((bwd_query_mfma_kernel<T, D>), grid, dim3(kThreads), 0, st, p,
-                         (const T*)q, (const T*)r, dy, conv_w, gamma, cu, (const float*)S,
-                         (const float*)z, dxt, dr, dsp, dgp);
+      if (gamma)
+        hipLaunchKernelGGL((bwd_query_mfma_kernel<T, D, true>), grid, dim3(kThreads), 0, st, p,
+                           (const T*)q, (const T*)r, dy, conv_w, gamma, cu, (const float*)S,
+                           (const float*)z, dxt, dr, dsp, dgp);
+      else
+        hipLaunchKernelGGL((bwd_query_mfma_kernel<T, D, false>), grid, dim3(kThreads), 0, st, p,
+                           (const T*)q, (const T*)r, dy, conv_w, gamma, cu, (const float*)S,
+                           (const float*)z, dxt, dr, dsp, dgp);
       hipLaunchKernelGGL((bwd_dscombine_kernel<D>), cgrid, dim3(kThreads), 0, st, p, cu,
                          (const float*)dsp, dS);
       hipLaunchKernelGGL((bwd_key_mfma_kernel<T, D>), grid, dim3(kThreads), 0, st, p,
@@ -1395,8 +1437,12 @@ gbla_status run_backward(const Plan& p, const BwdLayout& L, const void* q, const
                        (const T*)v, (const T*)a, conv_w, cu, dsp);
     gbla_status e = launch_combine_f32(p, cu, dsp, S, z, mz, st);
     if (e != GBLA_OK) return e;
-    hipLaunchKernelGGL((bwd_query_kernel<T, D>), grid, dim3(kThreads), 0, st, p, (const T*)q,
-                       (const T*)r, dy, conv_w, gamma, cu, S, z, dxt, dr, dsp, dgp);
+    if (gamma)
+      hipLaunchKernelGGL((bwd_query_kernel<T, D, true>), grid, dim3(kThreads), 0, st, p,
+                         (const T*)q, (const T*)r, dy, conv_w, gamma, cu, S, z, dxt, dr, dsp, dgp);
+    else
+      hipLaunchKernelGGL((bwd_query_kernel<T, D, false>), grid, dim3(kThreads), 0, st, p,
+                         (const T*)q, (const T*)r, dy, conv_w, gamma, cu, S, z, dxt, dr, dsp, dgp);
     hipLaunchKernelGGL((bwd_dscombine_kernel<D>), cgrid, dim3(kThreads), 0, st, p, cu,
                        (const float*)dsp, dS);
     hipLaunchKernelGGL((bwd_key_kernel<T, D>), grid, dim3(kThreads), 0, st, p, (const T*)k,

@@ -269,22 +269,29 @@ def backward_workspace_bytes(shape: Shape) -> int:
 
 def backward(q, k, v, gate_logits, out_gate, conv_w, norm_w, dy, eps: float = 1e-6,
              cu_seqlens=None, max_seqlen=None, workspace=None, stream=None,
-             grads: Optional[dict] = None) -> dict:
+             grads: Optional[dict] = None, flags: int = 0) -> dict:
     """Gradients of sum(forward(...) * dy) with respect to every input (fp32):
     a dict with dq, dk, dv, da (gate logits), dr (out gate), dconv_w, dgamma
     (norm weight), shaped like the inputs.  ``grads`` may hold preallocated
-    fp32 outputs under those names; they are overwritten."""
+    fp32 outputs under those names; they are overwritten.  Under the ablation
+    switches in ``flags`` the removed inputs may be None and their gradients
+    are left out of the dict."""
     _check_inputs(q, k, v, gate_logits, out_gate, conv_w, norm_w, cu_seqlens)
     dev = q.device
     _check(dy, "dy", torch.float32, dev)
     if dy.shape != q.shape:
         raise ValueError("dy must have the shape of q")
-    shape = make_shape(q, conv_w, eps, cu_seqlens, max_seqlen, 0)
+    shape = make_shape(q, conv_w, eps, cu_seqlens, max_seqlen, flags)
     if workspace is None:
         workspace = torch.empty(backward_workspace_bytes(shape), dtype=torch.uint8, device=dev)
     f32 = dict(dtype=torch.float32, device=dev)
-    want = {n: q.shape for n in ("dq", "dk", "dv", "dr")}
-    want.update(da=q.shape[:-1], dconv_w=conv_w.shape, dgamma=norm_w.shape)
+    want = {n: q.shape for n in ("dq", "dk", "dv")}
+    if not flags & NO_NORM:
+        want.update(dr=q.shape, dgamma=norm_w.shape)
+    if not flags & NO_GATE:
+        want.update(da=q.shape[:-1])
+    if not flags & NO_CONV:
+        want.update(dconv_w=conv_w.shape)
     g = dict(grads or {})
     for n, shp in want.items():
         if n not in g:
@@ -295,8 +302,8 @@ def backward(q, k, v, gate_logits, out_gate, conv_w, norm_w, dy, eps: float = 1e
     st = load_library().gbla_backward(
         ctypes.byref(shape), _ptr(q), _ptr(k), _ptr(v), _ptr(gate_logits), _ptr(out_gate),
         _ptr(conv_w), _ptr(norm_w), _ptr(cu_seqlens), _ptr(dy), _ptr(workspace), workspace.numel(),
-        _ptr(g["dq"]), _ptr(g["dk"]), _ptr(g["dv"]), _ptr(g["da"]), _ptr(g["dr"]),
-        _ptr(g["dconv_w"]), _ptr(g["dgamma"]), _stream(stream))
+        _ptr(g["dq"]), _ptr(g["dk"]), _ptr(g["dv"]), _ptr(g.get("da")), _ptr(g.get("dr")),
+        _ptr(g.get("dconv_w")), _ptr(g.get("dgamma")), _stream(stream))
     _raise(st, "gbla_backward")
     return g
 

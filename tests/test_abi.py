@@ -159,9 +159,16 @@ def test_backward_workspace_and_validation(lib):
     assert _backward(lib, s, ws=ALIGNED + 64) == 3
     assert _backward(lib, s, ws_bytes=3 * 8 * 32768 * 64 * 4) == 4   # the dq~, dk~, dv~ buffers alone
     assert _backward(lib, shape(head_dim=16)) == 2
-    for flags in (gbla.NO_GATE, gbla.NO_CONV, gbla.NO_NORM, gbla.BLA):
-        assert _backward(lib, shape(flags=flags)) == 2
     assert _backward(lib, shape(flags=8)) == 1
+    # switches: removed inputs and their gradients may be NULL (each call still
+    # stops at the missing workspace, which is checked last)
+    assert _backward(lib, shape(flags=gbla.NO_GATE), a=None, da=None, ws=None) == 4
+    assert _backward(lib, shape(flags=gbla.NO_CONV), w=None, dw=None, ws=None) == 4
+    assert _backward(lib, shape(flags=gbla.NO_NORM), r=None, g=None, dr=None, dg=None, ws=None) == 4
+    assert _backward(lib, shape(flags=gbla.BLA), a=None, da=None, w=None, dw=None, r=None, g=None,
+                     dr=None, dg=None, ws=None) == 4
+    assert _backward(lib, shape(flags=gbla.BLA), q=None, ws=None) == 1
+    assert _backward(lib, shape(flags=gbla.NO_NORM), dw=None, ws=None) == 1
 
 
 def lshape(**kw):

@@ -120,3 +120,35 @@ def test_backward_parity_full_size(G, dev, name):
     ref = gbla_backward.backward_inputs(inp, dy)
     for n in NAMES:
         close_scaled(got[n], ref[n], TOL[inp.workload.dtype], n)
+
+
+# Ablation switches (the paper's ablation table): each alone and all three
+# (BLA, Eq. (1)), through both kernel families (d = 32 / 64 on the matrix
+# cores, d = 128 on the vector path), dense and ragged.
+SWITCH_CASES = ["bf16_d64_n1000", "f32_d64_n1000", "ragged_d128_mixed", "bf16_d32_n3001_W2"]
+
+
+@pytest.mark.parametrize("sw", ["no_gate", "no_conv", "no_norm", "bla"])
+@pytest.mark.parametrize("name", SWITCH_CASES)
+def test_backward_switch_parity(G, dev, name, sw):
+    from oracle import gbla_backward
+    say("backward switch", sw, name)
+    w, lens = (SMALL_CASES[name], None) if name in SMALL_CASES else RAGGED_CASES[name]
+    flags = {"no_gate": G.NO_GATE, "no_conv": G.NO_CONV, "no_norm": G.NO_NORM, "bla": G.BLA}[sw]
+    gate, conv, norm = not flags & G.NO_GATE, not flags & G.NO_CONV, not flags & G.NO_NORM
+    inp = inputs.make_inputs(w, lengths=lens)
+    dy = inputs.make_cotangent(inp)
+    t = inputs.device_tensors(inp, dev)
+    # inputs a switch removes are passed as None: the library must not read
+    # them, nor write their gradients
+    g = G.backward(t["q"], t["k"], t["v"], t["a"] if gate else None, t["r"] if norm else None,
+                   t["conv_w"] if conv else None, t["gamma"] if norm else None,
+                   torch.from_numpy(dy).to(dev), eps=inp.eps, cu_seqlens=t["cu_seqlens"],
+                   max_seqlen=t["max_seqlen"], flags=flags)
+    torch.cuda.synchronize()
+    ref = gbla_backward.backward_inputs(inp, dy, gate=gate, conv=conv, norm=norm)
+    kept = ["dq", "dk", "dv"] + (["da"] if gate else []) + (["dconv_w"] if conv else [])
+    kept += ["dr", "dgamma"] if norm else []
+    assert sorted(g) == sorted(kept)
+    for n in kept:
+        close_scaled(g[n].cpu().numpy(), ref[n], TOL[w.dtype], n)

@@ -118,3 +118,29 @@ def test_rmsnorm_gradient_along_o_is_eps_sized():
         do = rs[:, None] * doh - (rs ** 3 / d * s1)[:, None] * o
         np.testing.assert_allclose(np.sum(do * o, axis=1), eps * rs ** 3 * s1,
                                    rtol=1e-9, atol=1e-12 * np.abs(rs * s1).max())
+
+
+def test_backward_without_the_gated_norm_matches_finite_differences(orc):
+    """norm=False is the layer with y = o (the ablation without gated RMSNorm):
+    its gradients against finite differences of the forward oracle's o."""
+    p, dy, meta = problem(61, W=3)
+    g = gbla_backward.backward(p["q"], p["k"], p["v"], p["a"], p["r"], p["conv_w"], p["gamma"],
+                               dy, norm=False, **meta)
+
+    def loss_o(pp):
+        o = orc.forward(pp["q"], pp["k"], pp["v"], pp["a"], pp["r"], pp["conv_w"], pp["gamma"],
+                        want=("o",), **meta)["o"]
+        return float(np.sum(o * dy))
+
+    rng = np.random.default_rng(2)
+    h = 1e-5
+    for name, gname in (("q", "dq"), ("k", "dk"), ("v", "dv"), ("a", "da"), ("conv_w", "dconv_w")):
+        x = p[name]
+        for flat in rng.choice(x.size, size=5, replace=False):
+            idx = np.unravel_index(flat, x.shape)
+            xp, xm = x.copy(), x.copy()
+            xp[idx] += h
+            xm[idx] -= h
+            fd = (loss_o(dict(p, **{name: xp})) - loss_o(dict(p, **{name: xm}))) / (2 * h)
+            assert abs(g[gname][idx] - fd) <= 1e-6 + 1e-5 * abs(fd), (gname, idx)
+    assert not g["dr"].any() and not g["dgamma"].any()
