@@ -301,9 +301,22 @@ def main():
     wall = time.perf_counter() - t0
     ms_per_step = ev0.elapsed_time(ev1) / args.steps
 
+    # Distribution of single forwards (events around each call, same rotation)
+    n_meas = min(args.steps, 200)
+    fwd_ev = []
+    for i in range(n_meas):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        step(i)
+        b.record(stream)
+        fwd_ev.append((a, b))
+    torch.cuda.synchronize()
+    fwd_us = sorted(1e3 * a.elapsed_time(b) for a, b in fwd_ev)
+    pct = {"p10": fwd_us[len(fwd_us) // 10], "p50": statistics.median(fwd_us),
+           "p90": fwd_us[(9 * len(fwd_us)) // 10]}
+
     # Live per-kernel timing of the dominant stage (the readout: 2/3 of the
     # algorithmic bytes), bracketed by events on the launch stream.
-    n_meas = min(args.steps, 200)
     pairs = []
     for i in range(n_meas):
         t = sets[i % nsets]
@@ -338,6 +351,7 @@ def main():
                    "inputs": w.dtype, "output": "f32", "rotating_sets": nsets,
                    "forward_effective_GBps": round(fwd_gbps, 1),
                    "forward_hbm_frac": round(fwd_gbps / HBM_PEAK_GBPS, 4),
+                   "single_forward_us": {k: round(v, 2) for k, v in pct.items()},
                    "wall_s": round(wall, 4)},
         "roofline": {"bound": "hbm", "kernel": "readout_stream_kernel", "achieved": round(ach, 1),
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBPS, 4),

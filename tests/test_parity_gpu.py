@@ -241,6 +241,37 @@ def test_deterministic(G, dev):
     assert torch.equal(y1, y2)
 
 
+def test_forward_under_graph_capture(G, dev):
+    """A captured forward replays correctly (its launches record no memset
+    and need no cleared workspace): every replay, with eager work and
+    synchronisations between them, equals the eager result."""
+    say("graph capture")
+    inp = inputs.make_inputs(SMALL_CASES["bf16_d64_n1000"])
+    t = inputs.device_tensors(inp, dev)
+    args = (t["q"], t["k"], t["v"], t["a"], t["r"], t["conv_w"], t["gamma"])
+    shape = G.make_shape(t["q"], t["conv_w"], inp.eps, None, None)
+    ws = G.alloc_workspace(shape, dev)
+    eager = G.forward(*args, eps=inp.eps, workspace=ws).clone()
+    out = torch.empty_like(eager)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        G.forward(*args, eps=inp.eps, workspace=ws, out=out)  # warm up on the side stream
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        G.forward(*args, eps=inp.eps, workspace=ws, out=out)
+    for i in range(3):
+        out.fill_(float("nan"))
+        other = G.forward(*args, eps=inp.eps, workspace=ws)  # eager work in between
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out, eager), "replay %d" % i
+        assert torch.equal(other, eager)
+
+
 def test_output_guard_canaries(G, dev):
     say("guard canaries")
     inp = inputs.make_inputs(small("b8_n2048_d64", batch=2, heads=2, seqlen=333, seed=41))
