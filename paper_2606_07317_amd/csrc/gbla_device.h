@@ -54,21 +54,28 @@ constexpr uint32_t kOutOfRange = 0x80000000u;
 
 // Taps of one tensor (0 = q, 1 = k, 2 = v), head h, channel c, right-aligned
 // to four taps: tap 3 multiplies the current token, taps before 4 - W are 0.
-// conv_w == NULL is the identity conv (the no-Conv1D switch).
+// conv_w == NULL is the identity conv (the no-Conv1D switch).  The loads go
+// through a buffer range over the taps (empty when conv_w is NULL), so there
+// is no branch around them: a branch would make the compiler wait for each
+// group of taps before issuing the loads that follow.
 __device__ __forceinline__ void load_taps4(const float* conv_w, int H, int h, int tensor, int D,
                                            int W, int c, float* w4) {
-  if (conv_w == nullptr) {
-    w4[0] = w4[1] = w4[2] = 0.0f;
-    w4[3] = 1.0f;
-    return;
-  }
-  const float* src = conv_w + (((size_t)tensor * H + h) * D + c) * W;
+  const __amdgpu_buffer_rsrc_t r =
+      make_rsrc(conv_w, conv_w ? (uint32_t)(3 * H * D * W) * 4u : 0u);
+  const uint32_t row = (uint32_t)(((tensor * H + h) * D + c) * W) * 4u;
+  if (W == 4) {  // one 16-byte load (W is wave-uniform)
+    const u32x4_t x = __builtin_amdgcn_raw_buffer_load_b128(r, row, 0, 0);
 #pragma unroll
-  for (int t = 0; t < 4; ++t) {
-    const int ti = t - (4 - W);
-    const float x = src[ti < 0 ? 0 : ti];  // unconditional load, then select
-    w4[t] = ti >= 0 ? x : 0.0f;
+    for (int t = 0; t < 4; ++t) w4[t] = __uint_as_float(x[t]);
+  } else {
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int ti = t - (4 - W);
+      w4[t] = __uint_as_float(
+          __builtin_amdgcn_raw_buffer_load_b32(r, ti >= 0 ? row + 4u * ti : kOutOfRange, 0, 0));
+    }
   }
+  w4[3] = conv_w ? w4[3] : 1.0f;
 }
 
 __device__ __forceinline__ float wave_max(float x) {

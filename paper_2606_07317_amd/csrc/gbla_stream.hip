@@ -470,11 +470,13 @@ readout_stream_kernel(Plan P, const uint16_t* __restrict__ qin, const uint16_t* 
   if (!unit_of(P, cu, P.rtile, P.rtiles_per_seq, g, &s, &tile)) return;
   s = __builtin_amdgcn_readfirstlane(s);
   tile = __builtin_amdgcn_readfirstlane(tile);
-  if (tid < D) {
-    load_taps4(conv_w, P.heads, h, 0, D, P.W, tid, taps_q[tid]);
-    gam[tid] = gamma ? gamma[(size_t)h * D + tid] : 1.0f;
-  }
-  __syncthreads();
+  // q taps and gamma of channel tid % D, loaded by every thread with no
+  // branch around the loads, so that the tile's first loads below are issued
+  // at once; the first D threads store them to LDS after those.
+  float tq[4];
+  load_taps4(conv_w, P.heads, h, 0, D, P.W, tid % D, tq);
+  const __amdgpu_buffer_rsrc_t rg = make_rsrc(gamma ? gamma + (size_t)h * D : gamma, gamma ? 4u * D : 0u);
+  const float graw = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rg, 4u * (tid % D), 0, 0));
   int64_t len, base_row;
   seq_geometry(P, cu, s, h, &len, &base_row);
   const int64_t tt0 = (int64_t)tile * P.rtile;
@@ -482,8 +484,7 @@ readout_stream_kernel(Plan P, const uint16_t* __restrict__ qin, const uint16_t* 
   const int per_wave = P.rtile >> 2;
   const int r0 = (int)(tt0 + (int64_t)wave * per_wave);  // slice-relative
   const int r1 = (int)min(tt1, (int64_t)r0 + per_wave);
-  if (r1 <= r0) return;  // no block-wide synchronisation follows
-  const int ngroups = (r1 - r0 + C::kGroup - 1) / C::kGroup;
+  const int ngroups = (r1 - r0 + C::kGroup - 1) / C::kGroup;  // < 1: the wave has no rows
   unsigned char* ring = lds + wave * C::kSlots * C::kSlotBytes;
 
   const int n = lane & 15, gq = lane >> 4;
@@ -505,15 +506,18 @@ readout_stream_kernel(Plan P, const uint16_t* __restrict__ qin, const uint16_t* 
     for (int kb = 0; kb < NKB; ++kb) A[mb][kb] = load16(fr + (((size_t)mb * NKB + kb) * 64 + lane) * 16);
 
   // ---- staged loads: q rows of a group, r chunks of the lane's two tokens ----
-  u32x4_t qst[C::kVec];
+  // Of the group before the wave's first token only rows 29..31 (the conv
+  // window) are read; they sit in the vectors from kXh on.
+  constexpr int kXh = (C::kGroup - 3) * C::kChunks / 64;
+  u32x4_t qst[C::kVec], qhalo[C::kVec - kXh];
   u32x4_t rst[2][NKB];
-  auto issue_q = [&](int grp, int first_row) {
+  auto issue_q = [&](u32x4_t(&dst)[C::kVec], int grp, int first_row) {
 #pragma unroll
     for (int x = 0; x < C::kVec; ++x) {
       const int u = x * 64 + lane;
       const int row = u / C::kChunks, ch = u % C::kChunks;
       const int tok = r0 + grp * C::kGroup + row;
-      qst[x] = bload16(rq, row >= first_row ? (uint32_t)(tok * D + ch * 8) * 2u : kOutOfRange);
+      dst[x] = bload16(rq, row >= first_row ? (uint32_t)(tok * D + ch * 8) * 2u : kOutOfRange);
     }
   };
   auto issue_r = [&](int grp, bool live) {
@@ -525,24 +529,44 @@ readout_stream_kernel(Plan P, const uint16_t* __restrict__ qin, const uint16_t* 
         rst[jb][qq] = bload16(rr, live ? (uint32_t)(tok * D + 32 * qq + 8 * gq) * 2u : kOutOfRange);
     }
   };
-  auto commit_q = [&](int grp) {
+  auto commit_q = [&](const u32x4_t(&src)[C::kVec], int grp) {
     const int slot = (grp + C::kSlots) % C::kSlots;
 #pragma unroll
     for (int x = 0; x < C::kVec; ++x) {
       const int u = x * 64 + lane;
       const int row = u / C::kChunks, ch = u % C::kChunks;
       *reinterpret_cast<u32x4_t*>(ring + slot * C::kSlotBytes + row * C::kRowBytes +
-                                  ((ch ^ (row & (C::kChunks - 1))) << 4)) = qst[x];
+                                  ((ch ^ (row & (C::kChunks - 1))) << 4)) = src[x];
     }
   };
 
-  // Rows 29..31 of the group before the wave's first token (the conv window).
-  issue_q(-1, C::kGroup - 3);
-  commit_q(-1);
-  issue_q(0, 0);
-  issue_r(0, true);
-  commit_q(0);
-  issue_q(1, ngroups > 1 ? 0 : C::kGroup);
+  // The conv window before the wave's first token, then group 0: both in
+  // flight before the first wait.
+#pragma unroll
+  for (int x = kXh; x < C::kVec; ++x) {
+    const int u = x * 64 + lane;
+    const int row = u / C::kChunks, ch = u % C::kChunks;
+    const int tok = r0 - C::kGroup + row;
+    qhalo[x - kXh] = bload16(rq, row >= C::kGroup - 3 ? (uint32_t)(tok * D + ch * 8) * 2u : kOutOfRange);
+  }
+  issue_q(qst, 0, 0);
+  if constexpr (kNorm) issue_r(0, true);
+  if (tid < D) {
+#pragma unroll
+    for (int t = 0; t < 4; ++t) taps_q[tid][t] = tq[t];
+    if constexpr (kNorm) gam[tid] = gamma ? graw : 1.0f;
+  }
+  __syncthreads();
+  if (ngroups < 1) return;  // no block-wide synchronisation follows
+#pragma unroll
+  for (int x = kXh; x < C::kVec; ++x) {
+    const int u = x * 64 + lane;
+    const int row = u / C::kChunks, ch = u % C::kChunks;
+    *reinterpret_cast<u32x4_t*>(ring + (C::kSlots - 1) * C::kSlotBytes + row * C::kRowBytes +
+                                ((ch ^ (row & (C::kChunks - 1))) << 4)) = qhalo[x - kXh];
+  }
+  commit_q(qst, 0);
+  issue_q(qst, 1, ngroups > 1 ? 0 : C::kGroup);
 
   for (int grp = 0; grp < ngroups; ++grp) {
     const unsigned char* cur = ring + (grp % C::kSlots) * C::kSlotBytes;
@@ -643,9 +667,9 @@ readout_stream_kernel(Plan P, const uint16_t* __restrict__ qin, const uint16_t* 
     // Stage group grp+1 into the ring (its slot held group grp-2), then
     // refill the registers: r of group grp+1 first, q rows of group grp+2
     // (fully out of range past the end, so the wait counts never change).
-    commit_q(grp + 1);
-    issue_r(grp + 1, grp + 1 < ngroups);
-    issue_q(grp + 2, grp + 2 < ngroups ? 0 : C::kGroup);
+    commit_q(qst, grp + 1);
+    if constexpr (kNorm) issue_r(grp + 1, grp + 1 < ngroups);
+    issue_q(qst, grp + 2, grp + 2 < ngroups ? 0 : C::kGroup);
   }
 }
 
