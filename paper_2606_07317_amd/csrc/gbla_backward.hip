@@ -391,17 +391,17 @@ bwd_dscombine_kernel(Plan P, const int32_t* __restrict__ cu, const float* __rest
   if (x >= kElems) return;
   const float* recs = dsp + ((size_t)h * P.units + first) * P.rec_floats + x;
   const size_t rf = P.rec_floats;
-  // in unit order; eight loads in flight per group
-  float acc = 0.0f;
+  // in unit order (compensated); eight loads in flight per group
+  float acc = 0.0f, cmp = 0.0f;
   int p = 0;
   for (; p + 8 <= count; p += 8) {
     float v[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) v[i] = recs[(size_t)(p + i) * rf];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) acc += v[i];
+    for (int i = 0; i < 8; ++i) kahan_add(acc, cmp, v[i]);
   }
-  for (; p < count; ++p) acc += recs[(size_t)p * rf];
+  for (; p < count; ++p) kahan_add(acc, cmp, recs[(size_t)p * rf]);
   dS[(size_t)sh_idx * kElems + x] = acc;
 }
 
@@ -587,7 +587,7 @@ bwd_param_kernel(Plan P, const int32_t* __restrict__ cu, const float* __restrict
   }
   const float* src = e < D ? dgp : dcp;
   const int u0 = (int)((int64_t)total * wave / 4), u1 = (int)((int64_t)total * (wave + 1) / 4);
-  float acc = 0.0f;
+  float acc = 0.0f, cmp = 0.0f;  // compensated: a quarter can hold thousands of units
   if (live) {
     int u = u0;
     for (; u + 8 <= u1; u += 8) {
@@ -595,9 +595,9 @@ bwd_param_kernel(Plan P, const int32_t* __restrict__ cu, const float* __restrict
 #pragma unroll
       for (int i = 0; i < 8; ++i) v[i] = src[off + (size_t)(u + i) * stride];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) acc += v[i];
+      for (int i = 0; i < 8; ++i) kahan_add(acc, cmp, v[i]);
     }
-    for (; u < u1; ++u) acc += src[off + (size_t)u * stride];
+    for (; u < u1; ++u) kahan_add(acc, cmp, src[off + (size_t)u * stride]);
   }
   red[wave][lane] = acc;
   __syncthreads();

@@ -78,6 +78,17 @@ __device__ __forceinline__ void load_taps4(const float* conv_w, int H, int h, in
   w4[3] = conv_w ? w4[3] : 1.0f;
 }
 
+// sum += x with Kahan's compensation: c carries the low-order bits that the
+// rounded sum lost, so a sum of n terms keeps an error of a few ulps instead
+// of growing with n.  Used for the fixed-order sums over chunks, which run to
+// thousands of terms on long sequences.
+__device__ __forceinline__ void kahan_add(float& sum, float& c, float x) {
+  const float y = x - c;
+  const float t = sum + y;
+  c = (t - sum) - y;
+  sum = t;
+}
+
 __device__ __forceinline__ float wave_max(float x) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) x = fmaxf(x, __shfl_xor(x, o));

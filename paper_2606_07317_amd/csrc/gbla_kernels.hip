@@ -432,8 +432,8 @@ __device__ __forceinline__ void frag_put(void* frag_sh, int mb, int kb, int lane
 // grid = (N * H, element slices of kThreads * E).  A block stages the chunk
 // weights w_p = exp(m_p - M) of its (sequence, head) in LDS and forms
 // Z = sum_p w_p l_p; each thread then sums element x of every partial in the
-// order p = 0, 1, ..., scales by 1/Z and writes S, z and the readout
-// fragments.  Every reduction order is fixed by the shape alone (not by E or
+// order p = 0, 1, ... (compensated, so that thousands of chunks keep the sum
+// to a few ulps), scales by 1/Z and writes S, z and the readout fragments.  Every reduction order is fixed by the shape alone (not by E or
 // the grid), so every call gives the same bits.
 constexpr int kCombineStage = 1024;  // chunk weights staged in LDS per round
 
@@ -499,12 +499,13 @@ combine_kernel(Plan P, const int32_t* __restrict__ cu, const float* __restrict__
   }
 
   int xe[E];
-  float v[E];
+  float v[E], cmp[E];  // compensated (Kahan) sums: sequences of thousands of chunks
 #pragma unroll
   for (int e = 0; e < E; ++e) {
     const int x = (blockIdx.y * E + e) * kThreads + tid;
     xe[e] = x < kElems ? x : 0;  // a valid address for every thread
     v[e] = 0.0f;
+    cmp[e] = 0.0f;
   }
   for (int p0 = 0; p0 < count; p0 += kCombineStage) {
     const int n = min(kCombineStage, count - p0);
@@ -524,7 +525,7 @@ combine_kernel(Plan P, const int32_t* __restrict__ cu, const float* __restrict__
       const float w = wst[p];
       const float* r = recs + (p0 + p) * rf;
 #pragma unroll
-      for (int e = 0; e < E; ++e) v[e] = fmaf(w, r[xe[e]], v[e]);
+      for (int e = 0; e < E; ++e) kahan_add(v[e], cmp[e], w * r[xe[e]]);
     }
   }
 

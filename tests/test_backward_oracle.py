@@ -144,3 +144,47 @@ def test_backward_without_the_gated_norm_matches_finite_differences(orc):
             fd = (loss_o(dict(p, **{name: xp})) - loss_o(dict(p, **{name: xm}))) / (2 * h)
             assert abs(g[gname][idx] - fd) <= 1e-6 + 1e-5 * abs(fd), (gname, idx)
     assert not g["dr"].any() and not g["dgamma"].any()
+
+
+def test_periodic_inputs_repeat_the_period(orc):
+    """The property the slice-limit GPU tests rest on, pinned on the oracles:
+    with q, k, v, a, r repeating with period P and the last W - 1 rows of
+    q, k, v zero in every period, y over m periods is y of one period
+    repeated; with dy repeating too, every per-token gradient over m periods
+    equals the two-period one (rows of periods 0..m-2 the first period, rows
+    of the last period the second), and dgamma and the taps' gradients scale
+    by m / 2."""
+    import dataclasses
+    from paper_2606_07317_amd import inputs
+    P, W, m = 48, 4, 5
+    w = inputs.Workload("period", batch=1, heads=2, seqlen=P, head_dim=8, conv_width=W,
+                        dtype=inputs.BF16, seed=52)
+    inp = inputs.make_inputs(w)
+    q, k, v = (x.copy() for x in (inp.q, inp.k, inp.v))
+    for x in (q, k, v):
+        x[:, :, P - (W - 1):, :] = 0
+    inp = dataclasses.replace(inp, q=q, k=k, v=v)
+
+    def rep(x, r):
+        return np.concatenate([x] * r, axis=2)
+
+    def repeated(r):
+        return dataclasses.replace(inp, workload=w.with_(seqlen=P * r), q=rep(inp.q, r),
+                                   k=rep(inp.k, r), v=rep(inp.v, r), a=rep(inp.a, r), r=rep(inp.r, r))
+
+    y1 = orc.forward_inputs(inp)["y"]
+    ym = orc.forward_inputs(repeated(m))["y"]
+    np.testing.assert_allclose(ym, rep(y1, m), rtol=1e-11, atol=1e-12)
+    dy = inputs.make_cotangent(inp)
+    g2 = gbla_backward.backward_inputs(repeated(2), rep(dy, 2))
+    gm = gbla_backward.backward_inputs(repeated(m), rep(dy, m))
+    for name in ("dq", "dk", "dv", "dr", "da"):
+        a2, am = g2[name], gm[name]
+        first, last = a2[:, :, :P], a2[:, :, P:]
+        for p in range(m):
+            want = last if p == m - 1 else first
+            np.testing.assert_allclose(am[:, :, p * P:(p + 1) * P], want, rtol=1e-9,
+                                       atol=1e-12 * np.abs(a2).max(), err_msg=name)
+    for name in ("dgamma", "dconv_w"):
+        np.testing.assert_allclose(gm[name], g2[name] * (m / 2.0), rtol=1e-9,
+                                   atol=1e-12 * np.abs(g2[name]).max(), err_msg=name)
