@@ -29,9 +29,12 @@ constexpr int kBM = 128, kBN = 128, kBK = 64;
 constexpr int kRowBytes = kBK * 2;           // one tile row of bf16
 constexpr int kTileBytes = 128 * kRowBytes;  // 16 KB
 
-// Byte offset of 16-byte chunk `c` of row `r` in a tile (chunks XOR-swizzled
-// by the row, so the MFMA operand reads of 32 rows spread over the banks).
-__device__ __forceinline__ int tile_off(int r, int c) { return r * kRowBytes + ((c ^ (r & 7)) << 4); }
+// Byte offset of 16-byte chunk `c` of row `r` in a tile.  The chunks are
+// XOR-swizzled by r / 2: a 16-byte operand read serves 16 lanes (16
+// consecutive rows) per cycle from 64 banks (256 bytes), and two rows share a
+// 256-byte bank row, so rows 2i and 2i + 1 take the two halves and the
+// swizzle spreads the eight pairs over the eight chunks.
+__device__ __forceinline__ int tile_off(int r, int c) { return r * kRowBytes + ((c ^ ((r >> 1) & 7)) << 4); }
 
 __device__ __forceinline__ u32x4_t bload(__amdgpu_buffer_rsrc_t r, uint32_t off) {
   return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
@@ -120,7 +123,13 @@ conv_x_kernel(LayerPlan P, const uint16_t* __restrict__ x, const float* __restri
 
 // ---------------------------------------------------------------------------
 // proj_kernel: P = Xt Wp^T on bf16 MFMA, scattered to the attention layout.
-// grid (features / 128, tokens / 128); 4 waves (2 x 2) of 64 x 64.
+// A 1-D grid of (features / 128) x (tokens / 128) tiles; 4 waves (2 x 2) of
+// 64 x 64.  When the token tiles come in multiples of 64, workgroup L goes to
+// XCD L % 8 (the dispatcher's round robin), and each XCD takes every eighth
+// token tile in groups of eight, walking all feature tiles of a group before
+// the next: the 64 workgroups an XCD holds at once then share eight token
+// tiles and eight feature tiles (about 4 MB, its L2), where the plain order
+// made every XCD stream all of Wp for every few token tiles.
 // ---------------------------------------------------------------------------
 __global__ void __launch_bounds__(kThreads, 2)
 proj_kernel(LayerPlan P, const uint16_t* __restrict__ xt, const uint16_t* __restrict__ wp,
@@ -129,27 +138,48 @@ proj_kernel(LayerPlan P, const uint16_t* __restrict__ xt, const uint16_t* __rest
   __shared__ __attribute__((aligned(16))) unsigned char lds[2][2][kTileBytes];  // [buf][Xt or W]
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
-  const int n0 = blockIdx.x * kBN, m0 = blockIdx.y * kBM;
+  const int tiles_n = (P.features + kBN - 1) / kBN, tiles_m = (P.tokens + kBM - 1) / kBM;
+  int tm, tn;
+  {
+    const int L = blockIdx.x;
+    if (tiles_m % 64 == 0) {
+      const int x = L % 8, j = L / 8, per = 8 * tiles_n;
+      const int grp = j / per, rr = j % per;
+      tn = rr / 8;
+      tm = (grp * 8 + rr % 8) * 8 + x;
+    } else {
+      tn = L % tiles_n;
+      tm = L / tiles_n;
+    }
+  }
+  const int n0 = tn * kBN, m0 = tm * kBM;
   const int K = P.d_model, M = P.tokens, N = P.features;
   const __amdgpu_buffer_rsrc_t rx = make_rsrc(xt, (uint32_t)((int64_t)M * K * 2));
   const __amdgpu_buffer_rsrc_t rw = make_rsrc(wp, (uint32_t)((int64_t)N * K * 2));
 
-  u32x4_t xraw[4], wraw[4];
-  auto issue = [&](int kt) {
+  const int nk = K / kBK;
+  // Register staging, two K steps ahead: set s holds the rows of every
+  // other step, so a step's rows have two steps of products to arrive.
+  u32x4_t xraw[2][4], wraw[2][4];
+  // Steps past the last load out of range (zeros, no traffic): the loads are
+  // never behind a branch, so the compiler's waits stay exact (a branch made
+  // it drain every load before each commit).
+  auto issue = [&](int set, int kt) {
     const int k0 = kt * kBK;
+    const bool live = kt < nk;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int c = tid + 256 * j, row = c >> 3, ch = c & 7;
-      xraw[j] = bload(rx, (uint32_t)(((int64_t)(m0 + row) * K + k0 + 8 * ch) * 2));
-      wraw[j] = bload(rw, (uint32_t)(((int64_t)(n0 + row) * K + k0 + 8 * ch) * 2));
+      xraw[set][j] = bload(rx, live ? (uint32_t)(((int64_t)(m0 + row) * K + k0 + 8 * ch) * 2) : kOutOfRange);
+      wraw[set][j] = bload(rw, live ? (uint32_t)(((int64_t)(n0 + row) * K + k0 + 8 * ch) * 2) : kOutOfRange);
     }
   };
-  auto commit = [&](int buf) {
+  auto commit = [&](int set, int buf) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int c = tid + 256 * j, row = c >> 3, ch = c & 7;
-      *reinterpret_cast<u32x4_t*>(&lds[buf][0][tile_off(row, ch)]) = xraw[j];
-      *reinterpret_cast<u32x4_t*>(&lds[buf][1][tile_off(row, ch)]) = wraw[j];
+      *reinterpret_cast<u32x4_t*>(&lds[buf][0][tile_off(row, ch)]) = xraw[set][j];
+      *reinterpret_cast<u32x4_t*>(&lds[buf][1][tile_off(row, ch)]) = wraw[set][j];
     }
   };
 
@@ -161,14 +191,8 @@ proj_kernel(LayerPlan P, const uint16_t* __restrict__ xt, const uint16_t* __rest
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
 
-  const int nk = K / kBK;
   const int half = lane >> 5, l32 = lane & 31;
-  issue(0);
-  commit(0);
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nk) issue(kt + 1);  // in flight during the products
+  auto products = [&](int buf) {
     const unsigned char* A = lds[buf][0];
     const unsigned char* B = lds[buf][1];
 #pragma unroll
@@ -187,7 +211,22 @@ proj_kernel(LayerPlan P, const uint16_t* __restrict__ xt, const uint16_t* __rest
                                                               __builtin_bit_cast(bf16x8_t, bf[j]),
                                                               acc[i][j], 0, 0, 0);
     }
-    if (kt + 1 < nk) commit(buf ^ 1);
+  };
+  // Step kt's rows sit in set kt % 2 and LDS buffer kt % 2; the loop runs two
+  // steps per turn so that every staging index is a constant.
+  issue(0, 0);
+  issue(1, 1);
+  commit(0, 0);
+  __syncthreads();
+  for (int kt = 0; kt < nk; kt += 2) {
+    issue(0, kt + 2);  // set 0 is free: step kt is in LDS
+    products(0);
+    commit(1, 1);      // zeros past the last step, never read
+    __syncthreads();
+    if (kt + 1 >= nk) break;
+    issue(1, kt + 3);
+    products(1);
+    commit(0, 0);
     __syncthreads();
   }
 
@@ -251,7 +290,7 @@ gbla_status launch_project(const LayerPlan& p, const void* x, const float* conv_
   if (p.tokens == 0) return GBLA_OK;
   hipLaunchKernelGGL(conv_x_kernel, dim3((p.d_model + 127) / 128, (p.tokens + 16 * kConvRun - 1) / (16 * kConvRun)),
                      dim3(kThreads), 0, st, p, (const uint16_t*)x, conv_x, cu, (uint16_t*)xt);
-  const dim3 grid((p.features + kBN - 1) / kBN, (p.tokens + kBM - 1) / kBM);
+  const dim3 grid((unsigned)(((p.features + kBN - 1) / kBN) * ((p.tokens + kBM - 1) / kBM)));
   hipLaunchKernelGGL(proj_kernel, grid, dim3(kThreads), 0, st, p, (const uint16_t*)xt,
                      (const uint16_t*)w_proj, (uint16_t*)q, (uint16_t*)k, (uint16_t*)v,
                      (uint16_t*)r, (uint16_t*)a);
