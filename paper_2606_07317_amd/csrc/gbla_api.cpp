@@ -140,11 +140,13 @@ gbla_status gbla_readout(const gbla_shape* shape, const void* q, const void* out
 }
 
 size_t gbla_backward_workspace_bytes(const gbla_shape* shape) {
-  Plan dense, ragged;
+  Plan dense, ragged, bd, br;
   if (gbla::make_plan(shape, false, &dense) != GBLA_OK) return 0;
   if (gbla::make_plan(shape, true, &ragged) != GBLA_OK) return 0;
-  const size_t a = gbla::make_bwd_layout(gbla::backward_plan(dense)).total_bytes;
-  const size_t b = gbla::make_bwd_layout(gbla::backward_plan(ragged)).total_bytes;
+  if (gbla::backward_plan(dense, &bd) != GBLA_OK) return 0;
+  if (gbla::backward_plan(ragged, &br) != GBLA_OK) return 0;
+  const size_t a = gbla::make_bwd_layout(bd).total_bytes;
+  const size_t b = gbla::make_bwd_layout(br).total_bytes;
   return a > b ? a : b;
 }
 
@@ -154,9 +156,9 @@ gbla_status gbla_backward(const gbla_shape* shape, const void* q, const void* k,
                           void* workspace, size_t workspace_bytes, float* dq, float* dk,
                           float* dv, float* d_gate_logits, float* d_out_gate, float* d_conv_w,
                           float* d_norm_w, void* stream) {
-  Plan p0;
+  Plan p0, p;
   GBLA_TRY(gbla::make_plan(shape, cu_seqlens != nullptr, &p0));
-  const Plan p = gbla::backward_plan(p0);
+  GBLA_TRY(gbla::backward_plan(p0, &p));
   // inputs a switch removes, and their gradients, are NULL inside the library
   gate_logits = unless(p, GBLA_NO_GATE, gate_logits);
   d_gate_logits = unless(p, GBLA_NO_GATE, d_gate_logits);

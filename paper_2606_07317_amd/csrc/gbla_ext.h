@@ -26,7 +26,7 @@ struct BwdLayout {
 };
 // The backward's plan: the forward's with its own unit size (the state
 // partials, dS partials and tap partials are per unit of this plan).
-Plan backward_plan(const Plan& p);
+gbla_status backward_plan(const Plan& p, Plan* out);
 BwdLayout make_bwd_layout(const Plan& p);
 
 // Backward launcher (gbla_backward.hip); dconv may be NULL (no Conv1D).

@@ -6,21 +6,25 @@
 
 namespace gbla {
 
-Plan backward_plan(const Plan& p) {
+gbla_status backward_plan(const Plan& p, Plan* out) {
   // Units of 512 tokens, whatever the forward's: long enough to amortise each
   // workgroup's set-up (A operands, the ordered wave sums), short enough for
   // two workgroups per CU at n = 32768, H = 8 (measured against 256 and 1024).
   Plan b = p;
   b.chunk = 512;
+  int64_t units;
   if (p.ragged) {
-    b.units = (int32_t)(b.tokens / b.chunk + b.nseq);
+    units = b.tokens / b.chunk + b.nseq;
   } else {
     int64_t cps = ((int64_t)b.rows + b.chunk - 1) / b.chunk;
     if (cps < 1) cps = 1;
     b.chunks_per_seq = (int32_t)cps;
-    b.units = (int32_t)(cps * b.nseq);
+    units = cps * b.nseq;
   }
-  return b;
+  if (units > 2147483647LL) return GBLA_ERR_UNSUPPORTED;  // the grid's x extent
+  b.units = (int32_t)units;
+  *out = b;
+  return GBLA_OK;
 }
 
 gbla_status make_layer_plan(const gbla_layer_shape* s, bool ragged, LayerPlan* p) {

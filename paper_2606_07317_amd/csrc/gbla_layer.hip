@@ -288,9 +288,11 @@ gbla_status launch_project(const LayerPlan& p, const void* x, const float* conv_
                            const void* w_proj, const int32_t* cu, void* xt, void* q, void* k,
                            void* v, void* r, void* a, hipStream_t st) {
   if (p.tokens == 0) return GBLA_OK;
+  const int64_t tiles = (int64_t)((p.features + kBN - 1) / kBN) * ((p.tokens + kBM - 1) / kBM);
+  if (tiles > 2147483647LL) return GBLA_ERR_UNSUPPORTED;  // the grid's x extent; nothing enqueued
   hipLaunchKernelGGL(conv_x_kernel, dim3((p.d_model + 127) / 128, (p.tokens + 16 * kConvRun - 1) / (16 * kConvRun)),
                      dim3(kThreads), 0, st, p, (const uint16_t*)x, conv_x, cu, (uint16_t*)xt);
-  const dim3 grid((unsigned)(((p.features + kBN - 1) / kBN) * ((p.tokens + kBM - 1) / kBM)));
+  const dim3 grid((unsigned)tiles);
   hipLaunchKernelGGL(proj_kernel, grid, dim3(kThreads), 0, st, p, (const uint16_t*)xt,
                      (const uint16_t*)w_proj, (uint16_t*)q, (uint16_t*)k, (uint16_t*)v,
                      (uint16_t*)r, (uint16_t*)a);
