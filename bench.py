@@ -315,6 +315,25 @@ def main():
     pct = {"p10": fwd_us[len(fwd_us) // 10], "p50": statistics.median(fwd_us),
            "p90": fwd_us[(9 * len(fwd_us)) // 10]}
 
+    # Practical ceiling: a device-to-device copy moving the forward's
+    # algorithmic bytes (half read, half written), over as many rotating
+    # buffers as the forward uses, timed the same way.
+    half = algorithmic_bytes(inp, "forward") // 2 // 4
+    bufs = [torch.empty(half, dtype=torch.float32, device=dev) for _ in range(nsets + 1)]
+    for b in bufs:
+        b.fill_(1.0)
+    cp = []
+    for i in range(n_meas):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        bufs[(i + 1) % len(bufs)].copy_(bufs[i % len(bufs)])
+        b.record(stream)
+        cp.append((a, b))
+    torch.cuda.synchronize()
+    copy_us = statistics.median(1e3 * a.elapsed_time(b) for a, b in cp)
+    copy_gbps = 8 * half / (copy_us * 1e-6) / 1e9
+    del bufs
+
     # Live per-kernel timing of the dominant stage (the readout: 2/3 of the
     # algorithmic bytes), bracketed by events on the launch stream.
     pairs = []
@@ -352,6 +371,9 @@ def main():
                    "forward_effective_GBps": round(fwd_gbps, 1),
                    "forward_hbm_frac": round(fwd_gbps / HBM_PEAK_GBPS, 4),
                    "single_forward_us": {k: round(v, 2) for k, v in pct.items()},
+                   "copy_same_bytes_us": round(copy_us, 2),
+                   "copy_same_bytes_GBps": round(copy_gbps, 1),
+                   "forward_over_copy": round(copy_us / pct["p50"], 4),
                    "wall_s": round(wall, 4)},
         "roofline": {"bound": "hbm", "kernel": "readout_stream_kernel", "achieved": round(ach, 1),
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBPS, 4),
