@@ -82,8 +82,11 @@ def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
     """Round fp32 values to bf16 (round-to-nearest-even) and return the raw
     16-bit patterns as uint16.  Inputs here are finite normals; NaN is kept NaN."""
     x = np.ascontiguousarray(x, dtype=np.float32)
-    u = x.view(np.uint32).astype(np.uint64)
-    rounded = ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
+    # 32-bit arithmetic does not wrap for finite or infinite patterns (at most
+    # 0xFF800000 + 0x8000); NaN patterns, which could, are replaced below.
+    u = x.view(np.uint32)
+    rounded = ((u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1)))
+               >> np.uint32(16)).astype(np.uint16)
     nan = np.isnan(x)
     if nan.any():
         rounded[nan] = 0x7FC0

@@ -118,3 +118,28 @@ def test_layer_forward_full_size_table5(G, dev, orc):
     say("  y max abs %.3e, worst err/tol %.3f" % (err.max(), (err / (2e-2 * (1 + np.abs(ref)))).max()))
     assert np.isfinite(got).all()
     assert (err <= 2e-2 * (1 + np.abs(ref))).all()
+
+
+def test_layer_forward_full_size_long_sampled(G, dev, orc):
+    """The bench's layer workload (Table 5's layer at L = 32768, batch 8) in
+    its launch configuration: sequences 0 and 7 of the full batch against the
+    oracle run on those two sequences alone (every output of a sequence
+    depends on that sequence only)."""
+    import dataclasses
+    from oracle import gbla_layer
+    w = inputs.LAYER_WORKLOADS["layer_b8_n32768"]
+    say("layer forward full size, sampled", w.name)
+    inp = inputs.make_layer_inputs(w)
+    t = inputs.layer_device_tensors(inp, dev)
+    y = G.layer_forward(t["x"], t["conv_x"], t["w_proj"], t["gamma"], eps=w.eps)
+    torch.cuda.synchronize()
+    pick = [0, 7]
+    got = y[pick].cpu().numpy().astype(np.float64)
+    del y, t
+    sub = dataclasses.replace(inp, workload=w.with_(batch=len(pick)), x=inp.x[pick])
+    ref = gbla_layer.layer_forward(orc, sub.x, sub.conv_x, sub.w_proj, sub.gamma, eps=w.eps,
+                                   rounding=True, **oracle_meta(sub))["y"]
+    err = np.abs(got - ref)
+    say("  y max abs %.3e, worst err/tol %.3f" % (err.max(), (err / (2e-2 * (1 + np.abs(ref)))).max()))
+    assert np.isfinite(got).all()
+    assert (err <= 2e-2 * (1 + np.abs(ref))).all()
