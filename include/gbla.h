@@ -153,6 +153,21 @@ gbla_status gbla_readout(const gbla_shape* shape, const void* q, const void* out
                          size_t workspace_bytes, float* out, void* stream);
 
 /*
+ * gbla_readout, with the readout kernel's own duration: start_event and
+ * stop_event (hipEvent_t, created by the caller, either may be NULL) are
+ * recorded when the kernel begins executing and when it ends, as
+ * hipExtLaunchKernel does, so hipEventElapsedTime gives the kernel's time
+ * without the launch gaps that events recorded around the call would add.
+ * With no tokens nothing is launched and both events are recorded on the
+ * stream.  Results, argument checks and errors are gbla_readout's.
+ */
+gbla_status gbla_readout_timed(const gbla_shape* shape, const void* q, const void* out_gate,
+                               const float* conv_w, const float* norm_w,
+                               const int32_t* cu_seqlens, void* workspace,
+                               size_t workspace_bytes, float* out, void* stream,
+                               void* start_event, void* stop_event);
+
+/*
  * Bytes of device scratch that gbla_backward needs for this shape (dense or
  * ragged); 0 for an invalid shape.  About 12 * tokens * H * d bytes (fp32
  * gradients of the convolved q, k, v) plus per-chunk partials.

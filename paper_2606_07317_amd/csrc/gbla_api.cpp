@@ -123,9 +123,11 @@ gbla_status gbla_state(const gbla_shape* shape, const void* k, const void* v,
                             static_cast<hipStream_t>(stream));
 }
 
-gbla_status gbla_readout(const gbla_shape* shape, const void* q, const void* out_gate,
-                         const float* conv_w, const float* norm_w, const int32_t* cu_seqlens,
-                         void* workspace, size_t workspace_bytes, float* out, void* stream) {
+static gbla_status readout_entry(const gbla_shape* shape, const void* q, const void* out_gate,
+                                 const float* conv_w, const float* norm_w,
+                                 const int32_t* cu_seqlens, void* workspace,
+                                 size_t workspace_bytes, float* out, void* stream,
+                                 gbla::KernelEvents ev) {
   Plan p;
   GBLA_TRY(gbla::make_plan(shape, cu_seqlens != nullptr, &p));
   conv_w = unless(p, GBLA_NO_CONV, conv_w);
@@ -136,7 +138,26 @@ gbla_status gbla_readout(const gbla_shape* shape, const void* q, const void* out
   if (!(p.flags & GBLA_NO_NORM)) GBLA_TRY(check_used({out_gate, norm_w}));
   GBLA_TRY(check_ws(p, workspace, workspace_bytes));
   return gbla::launch_readout(p, q, out_gate, conv_w, norm_w, cu_seqlens, workspace, out,
-                              static_cast<hipStream_t>(stream));
+                              static_cast<hipStream_t>(stream), ev);
+}
+
+gbla_status gbla_readout(const gbla_shape* shape, const void* q, const void* out_gate,
+                         const float* conv_w, const float* norm_w, const int32_t* cu_seqlens,
+                         void* workspace, size_t workspace_bytes, float* out, void* stream) {
+  return readout_entry(shape, q, out_gate, conv_w, norm_w, cu_seqlens, workspace,
+                       workspace_bytes, out, stream, {});
+}
+
+gbla_status gbla_readout_timed(const gbla_shape* shape, const void* q, const void* out_gate,
+                               const float* conv_w, const float* norm_w,
+                               const int32_t* cu_seqlens, void* workspace,
+                               size_t workspace_bytes, float* out, void* stream,
+                               void* start_event, void* stop_event) {
+  gbla::KernelEvents ev;
+  ev.start = static_cast<hipEvent_t>(start_event);
+  ev.stop = static_cast<hipEvent_t>(stop_event);
+  return readout_entry(shape, q, out_gate, conv_w, norm_w, cu_seqlens, workspace,
+                       workspace_bytes, out, stream, ev);
 }
 
 size_t gbla_backward_workspace_bytes(const gbla_shape* shape) {

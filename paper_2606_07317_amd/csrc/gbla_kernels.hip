@@ -27,6 +27,7 @@
 // Data types: activations are fp32 or bf16 (raw 16-bit patterns); all
 // arithmetic is fp32 except the MFMA operands of the bf16 path, which are
 // rounded to bf16 (round to nearest even) and accumulated in fp32.
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -877,13 +878,23 @@ template <typename T, int D>
 struct ReadoutRun {
   static gbla_status run(const Plan& p, const void* q, const void* r, const float* w,
                          const float* gamma, const int32_t* cu, const void* ws, float* out,
-                         hipStream_t st) {
-    if (p.tokens == 0) return GBLA_OK;
+                         hipStream_t st, KernelEvents ev) {
+    if (p.tokens == 0) {
+      // nothing to launch: the events still mark this point of the stream
+      if (ev.start && hipEventRecord(ev.start, st) != hipSuccess) return GBLA_ERR_HIP;
+      if (ev.stop && hipEventRecord(ev.stop, st) != hipSuccess) return GBLA_ERR_HIP;
+      return GBLA_OK;
+    }
     const unsigned char* base = static_cast<const unsigned char*>(ws);
     if (stream_supported(p))
-      return launch_readout_stream(p, q, r, w, gamma, cu, base + p.off_frags, out, st);
-    hipLaunchKernelGGL((readout_kernel<T, D>), dim3(p.runits, p.heads), dim3(kThreads), 0, st,
-                       p, (const T*)q, (const T*)r, w, gamma, cu, base + p.off_frags, out);
+      return launch_readout_stream(p, q, r, w, gamma, cu, base + p.off_frags, out, st, ev);
+    if (ev.any())
+      hipExtLaunchKernelGGL((readout_kernel<T, D>), dim3(p.runits, p.heads), dim3(kThreads), 0, st,
+                            ev.start, ev.stop, 0, p, (const T*)q, (const T*)r, w, gamma, cu,
+                            base + p.off_frags, out);
+    else
+      hipLaunchKernelGGL((readout_kernel<T, D>), dim3(p.runits, p.heads), dim3(kThreads), 0, st,
+                         p, (const T*)q, (const T*)r, w, gamma, cu, base + p.off_frags, out);
     return last_launch_status();
   }
 };
@@ -909,8 +920,8 @@ gbla_status launch_combine_f32(const Plan& p, const int32_t* cu, const float* pa
 
 gbla_status launch_readout(const Plan& p, const void* q, const void* r, const float* conv_w,
                            const float* gamma, const int32_t* cu, const void* workspace,
-                           float* out, hipStream_t stream) {
-  return dispatch<ReadoutRun>(p, q, r, conv_w, gamma, cu, workspace, out, stream);
+                           float* out, hipStream_t stream, KernelEvents ev) {
+  return dispatch<ReadoutRun>(p, q, r, conv_w, gamma, cu, workspace, out, stream, ev);
 }
 
 }  // namespace gbla

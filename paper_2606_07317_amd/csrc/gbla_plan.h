@@ -53,6 +53,16 @@ gbla_status make_plan(const gbla_shape* s, bool ragged, Plan* p);
 size_t align_up(size_t x, size_t a);
 bool aligned(const void* p, size_t a);
 
+// Optional kernel-duration events for the readout launch.  When either is
+// set, the kernel goes through hipExtLaunchKernel, which records `start` as
+// the kernel begins executing and `stop` as it ends, so their elapsed time is
+// the kernel's own duration, without the launch gaps around it.
+struct KernelEvents {
+  hipEvent_t start = nullptr;
+  hipEvent_t stop = nullptr;
+  bool any() const { return start != nullptr || stop != nullptr; }
+};
+
 // Kernel launchers (gbla_kernels.hip).  Arguments were validated by the
 // caller; these only enqueue work on `stream`.
 gbla_status launch_conv(const Plan& p, const void* q, const void* k, const void* v,
@@ -65,7 +75,7 @@ gbla_status launch_state(const Plan& p, const void* k, const void* v, const void
                          float* S, float* z, float* mz, hipStream_t stream);
 gbla_status launch_readout(const Plan& p, const void* q, const void* r, const float* conv_w,
                            const float* gamma, const int32_t* cu, const void* workspace,
-                           float* out, hipStream_t stream);
+                           float* out, hipStream_t stream, KernelEvents ev = {});
 // The fixed-order combine of partial records [S_p | z_p | m_p | l_p] laid out
 // like the forward's (rec_floats apart, [H, units]), with full-accuracy expf
 // for every dtype and no readout operands: S, z, mz as in launch_state.
@@ -79,6 +89,6 @@ gbla_status launch_state_stream(const Plan& p, const void* k, const void* v, con
                                 hipStream_t stream);
 gbla_status launch_readout_stream(const Plan& p, const void* q, const void* r, const float* conv_w,
                                   const float* gamma, const int32_t* cu, const unsigned char* frags,
-                                  float* out, hipStream_t stream);
+                                  float* out, hipStream_t stream, KernelEvents ev = {});
 
 }  // namespace gbla

@@ -35,6 +35,7 @@
 // past its end read as zero, stores past the tile end are dropped.  There
 // are no branches around memory instructions, so the compiler's wait counts
 // stay exact and the prefetched loads remain in flight.
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -703,12 +704,18 @@ gbla_status launch_state_stream(const Plan& p, const void* k, const void* v, con
 
 gbla_status launch_readout_stream(const Plan& p, const void* q, const void* r, const float* conv_w,
                                   const float* gamma, const int32_t* cu, const unsigned char* frags,
-                                  float* out, hipStream_t st) {
+                                  float* out, hipStream_t st, KernelEvents ev) {
   const dim3 grid(p.runits, p.heads);
   const uint16_t *qq = (const uint16_t*)q, *rr = (const uint16_t*)r;
-#define GBLA_READOUT(DD, NORM)                                                             \
-  hipLaunchKernelGGL((readout_stream_kernel<DD, NORM>), grid, dim3(kThreads), 0, st, p, qq, rr, \
-                     conv_w, gamma, cu, frags, out)
+#define GBLA_READOUT(DD, NORM)                                                                \
+  do {                                                                                        \
+    if (ev.any())                                                                             \
+      hipExtLaunchKernelGGL((readout_stream_kernel<DD, NORM>), grid, dim3(kThreads), 0, st,   \
+                            ev.start, ev.stop, 0, p, qq, rr, conv_w, gamma, cu, frags, out);  \
+    else                                                                                      \
+      hipLaunchKernelGGL((readout_stream_kernel<DD, NORM>), grid, dim3(kThreads), 0, st, p,   \
+                         qq, rr, conv_w, gamma, cu, frags, out);                              \
+  } while (0)
   const bool norm = gamma != nullptr;  // NULL gamma: the no-gated-norm switch
   if (p.d == 128) {
     if (norm) GBLA_READOUT(128, true); else GBLA_READOUT(128, false);

@@ -74,6 +74,8 @@ def load_library(path: str = LIB_PATH):
     lib.gbla_state.restype = ctypes.c_int
     lib.gbla_readout.argtypes = [SP, P, P, P, P, P, P, sz, P, P]
     lib.gbla_readout.restype = ctypes.c_int
+    lib.gbla_readout_timed.argtypes = [SP, P, P, P, P, P, P, sz, P, P, P, P]
+    lib.gbla_readout_timed.restype = ctypes.c_int
     lib.gbla_backward_workspace_bytes.argtypes = [SP]
     lib.gbla_backward_workspace_bytes.restype = sz
     lib.gbla_backward.argtypes = [SP, P, P, P, P, P, P, P, P, P, P, sz, P, P, P, P, P, P, P, P]
@@ -246,17 +248,25 @@ def state(k, v, gate_logits, conv_w, cu_seqlens=None, max_seqlen=None, workspace
 
 
 def readout(q, out_gate, conv_w, norm_w, workspace, eps: float = 1e-6, cu_seqlens=None,
-            max_seqlen=None, out=None, stream=None, flags: int = 0) -> torch.Tensor:
+            max_seqlen=None, out=None, stream=None, flags: int = 0,
+            kernel_events=None) -> torch.Tensor:
     """Readout + gated RMSNorm from the state a preceding state() call left in
-    ``workspace``."""
+    ``workspace``.  ``kernel_events`` = (start, stop) torch.cuda.Events that
+    are recorded when the readout kernel begins and ends (gbla_readout_timed);
+    each must have been recorded once before, so that its HIP event exists."""
     _check_inputs(q, None, None, None, out_gate, conv_w, norm_w, cu_seqlens)
     shape = make_shape(q, conv_w, eps, cu_seqlens, max_seqlen, flags)
     if out is None:
         out = torch.empty(q.shape, dtype=torch.float32, device=q.device)
-    st = load_library().gbla_readout(ctypes.byref(shape), _ptr(q), _ptr(out_gate), _ptr(conv_w),
-                                     _ptr(norm_w), _ptr(cu_seqlens), _ptr(workspace),
-                                     workspace.numel(), _ptr(out), _stream(stream))
-    _raise(st, "gbla_readout")
+    args = (ctypes.byref(shape), _ptr(q), _ptr(out_gate), _ptr(conv_w), _ptr(norm_w),
+            _ptr(cu_seqlens), _ptr(workspace), workspace.numel(), _ptr(out), _stream(stream))
+    if kernel_events is None:
+        _raise(load_library().gbla_readout(*args), "gbla_readout")
+    else:
+        handles = [e.cuda_event for e in kernel_events]
+        if not all(handles):
+            raise ValueError("kernel_events must have been recorded once before")
+        _raise(load_library().gbla_readout_timed(*args, *handles), "gbla_readout_timed")
     return out
 
 

@@ -27,7 +27,7 @@ def shape(**kw):
 def test_exports_every_declared_function(lib):
     names = gbla.declared_functions()
     assert {"gbla_forward", "gbla_workspace_bytes", "gbla_conv1d", "gbla_state",
-            "gbla_readout", "gbla_status_string", "gbla_backward",
+            "gbla_readout", "gbla_readout_timed", "gbla_status_string", "gbla_backward",
             "gbla_backward_workspace_bytes", "gbla_layer_workspace_bytes", "gbla_layer_project",
             "gbla_layer_forward"} <= set(names)
     for n in names:
@@ -103,6 +103,9 @@ def test_other_entry_points_reject_before_launch(lib):
     assert lib.gbla_readout(ctypes.byref(s), None, P, P, P, None, P, 1 << 40, P, None) == 1
     assert lib.gbla_readout(ctypes.byref(s), P, P, P, P, None, None, 1 << 40, P, None) == 4
     assert lib.gbla_readout(ctypes.byref(s), P, P, P, P, None, P, 0, P, None) == 4
+    # the timed variant checks its arguments as gbla_readout does, events aside
+    assert lib.gbla_readout_timed(ctypes.byref(s), None, P, P, P, None, P, 1 << 40, P, None, P, P) == 1
+    assert lib.gbla_readout_timed(ctypes.byref(s), P, P, P, P, None, P, 0, P, None, None, None) == 4
 
 
 def test_ablation_switches_validation(lib):

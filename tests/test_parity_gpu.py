@@ -230,6 +230,33 @@ def test_state_then_readout_equals_forward(G, dev):
     assert torch.equal(y, y2)
 
 
+@pytest.mark.parametrize("name", ["bf16_d64_n1000", "f32_d64_n1000"])
+def test_timed_readout_equals_readout(G, dev, name):
+    """gbla_readout_timed gives gbla_readout's bits, and the events the launch
+    records bracket the kernel alone: a positive time within that of events
+    recorded around the call."""
+    say("timed readout, " + name)
+    inp = inputs.make_inputs(SMALL_CASES[name])
+    t = inputs.device_tensors(inp, dev)
+    shape = G.make_shape(t["q"], t["conv_w"], inp.eps, None, None)
+    ws = G.alloc_workspace(shape, dev)
+    G.state(t["k"], t["v"], t["a"], t["conv_w"], workspace=ws)
+    y = G.readout(t["q"], t["r"], t["conv_w"], t["gamma"], ws, eps=inp.eps)
+    stream = torch.cuda.current_stream()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    for e in ev[:2]:
+        e.record(stream)
+    ev[2].record(stream)
+    y2 = G.readout(t["q"], t["r"], t["conv_w"], t["gamma"], ws, eps=inp.eps,
+                   kernel_events=(ev[0], ev[1]))
+    ev[3].record(stream)
+    torch.cuda.synchronize()
+    assert torch.equal(y, y2)
+    kernel_ms, call_ms = ev[0].elapsed_time(ev[1]), ev[2].elapsed_time(ev[3])
+    say("  kernel %.2f us, call %.2f us" % (1e3 * kernel_ms, 1e3 * call_ms))
+    assert 0.0 < kernel_ms <= call_ms
+
+
 def test_deterministic(G, dev):
     say("determinism")
     inp = inputs.make_inputs(small("b8_n2048_d64", batch=2, heads=4, seqlen=5000, seed=40))
