@@ -260,6 +260,45 @@ def test_readout_matches_quadratic_bruteforce(orc, n):
             np.testing.assert_allclose(out["y"][s, h], y, rtol=1e-12, atol=1e-14)
 
 
+def torch_gbla(q, k, v, a, r, conv_w, gamma, eps):
+    """GBLA of one batch [B, H, n, d] composed from torch fp64 CPU library
+    operators (Section 2.1): a grouped (depthwise) conv1d with W - 1 zeros of
+    left padding, elu + 1, softmax over the tokens, matrix products for the
+    state and the readout, and the gated RMSNorm with torch's silu."""
+    import torch
+    import torch.nn.functional as F
+
+    t = lambda x: torch.from_numpy(np.ascontiguousarray(x)).double()
+    q, k, v, a, r, conv_w, gamma = map(t, (q, k, v, a, r, conv_w, gamma))
+    B, H, n, d = q.shape
+    W = conv_w.shape[-1]
+
+    def conv(x, taps):  # x [B, H, n, d], taps [H, d, W] (tap W - 1 = current token)
+        xc = x.permute(0, 1, 3, 2).reshape(B, H * d, n)
+        y = F.conv1d(F.pad(xc, (W - 1, 0)), taps.reshape(H * d, 1, W), groups=H * d)
+        return y.reshape(B, H, d, n).permute(0, 1, 3, 2)
+
+    qt, kt, vt = conv(q, conv_w[0]), conv(k, conv_w[1]), conv(v, conv_w[2])
+    Qh, Kh = F.elu(qt) + 1.0, F.elu(kt) + 1.0
+    g = torch.softmax(a, dim=-1)                        # [B, H, n]
+    S = (Kh * g[..., None]).transpose(-1, -2) @ vt      # [B, H, d, d]
+    z = (Kh * g[..., None]).sum(-2)                     # [B, H, d]
+    o = (Qh @ S) / (Qh @ z[..., None])
+    oh = o * torch.rsqrt((o * o).mean(-1, keepdim=True) + eps)
+    return (oh * gamma[None, :, None, :] * F.silu(r)).numpy()
+
+
+@pytest.mark.parametrize("W", [1, 4])
+def test_torch_fp64_composition_agrees(orc, W):
+    """An independent composition from torch's CPU operators gives the
+    oracle's y to 1e-12 (dense; ragged batches reduce to dense slices by
+    test_conv_does_not_cross_sequences)."""
+    p = rand_problem(90 + W, nseq=2, H=3, n=37, d=6, W=W)
+    out = run(orc, p, eps=1e-5, want=("y",))
+    ref = torch_gbla(p["q"], p["k"], p["v"], p["a"], p["r"], p["conv_w"], p["gamma"], 1e-5)
+    np.testing.assert_allclose(out["y"], ref, rtol=1e-12, atol=1e-14)
+
+
 def test_single_token_returns_its_value(orc):
     p = rand_problem(30, nseq=3, H=2, n=1, d=6, W=4)
     out = run(orc, p, want=("o", "vt"))
