@@ -213,7 +213,7 @@ def bench_layer(args, inp, dev):
                       "tokens_per_s": tokens / (ms * 1e-3), "rotating_sets": nsets,
                       "paper_h100_ms": PAPER_H100_LAYER_MS.get(w.seqlen),
                       "wall_s": round(wall, 4)},
-           "roofline": {"bound": "mfma", "kernel": "proj_kernel", "achieved": round(tfl, 1),
+           "roofline": {"bound": "mfma", "kernel": "conv_x_kernel+proj_kernel", "achieved": round(tfl, 1),
                         "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                         "frac": round(tfl / MFMA_BF16_PEAK_TFLOPS, 4), "avg_launch_ms": proj_ms,
                         "traffic": None}}
