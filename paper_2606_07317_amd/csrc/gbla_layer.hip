@@ -27,6 +27,7 @@ namespace {
 
 constexpr int kBM = 256, kBN = 256, kBK = 32;
 constexpr int kProjWaves = 8, kProjThreads = 64 * kProjWaves;  // 2 x 4 waves
+constexpr int kProjGrid = 256;                                  // persistent workgroups
 constexpr int kWaveM = kBM / 2, kWaveN = kBN / 4;               // 128 x 64 per wave
 constexpr int kRowBytes = kBK * 2;           // one tile row of bf16: four 16-byte chunks
 constexpr int kTileBytes = 256 * kRowBytes;  // 16 KB
@@ -144,16 +145,18 @@ conv_x_kernel(LayerPlan P, const uint16_t* __restrict__ x, const float* __restri
 
 // ---------------------------------------------------------------------------
 // proj_kernel: P = Xt Wp^T on bf16 MFMA, scattered to the attention layout.
-// A 1-D grid of (features / 256) x (tokens / 256) tiles; 8 waves (2 x 4) of
-// 128 x 64, two per SIMD.  A wave tile of 128 x 64 reads 0.75 KB of LDS
-// operands per 32x32x16 product, against 1 KB for 64 x 64, and the larger
-// workgroup tile halves the L2 reads per product; the 128 KB of LDS (two K
-// steps of both tiles) keeps one workgroup per CU.  When the token tiles come
-// in multiples of 64, workgroup L goes to XCD L % 8 (the dispatcher's round
-// robin), and each XCD takes every eighth token tile in groups of eight,
-// walking all feature tiles of a group before the next, so that the
-// workgroups an XCD holds at once share a few token and feature tiles in its
-// L2, where the plain order made every XCD stream all of Wp.
+// (features / 256) x (tokens / 256) tiles, numbered L, owned by persistent
+// workgroups (tiles blockIdx.x, blockIdx.x + gridDim.x, ...); 8 waves
+// (2 x 4) of 128 x 64, two per SIMD, so one workgroup per CU (244 VGPRs a
+// wave).  A wave tile of 128 x 64 reads 0.75 KB of LDS operands per 32x32x16
+// product, against 1 KB for 64 x 64, and the larger workgroup tile halves
+// the L2 reads per product.  The dispatcher places workgroup b on XCD b % 8;
+// with a grid that is a multiple of 8, tile L therefore runs on XCD L % 8.
+// When the token tiles come in multiples of 64, each XCD takes every eighth
+// token tile in groups of eight, walking all feature tiles of a group before
+// the next, so that the workgroups an XCD holds at once share a few token
+// and feature tiles in its L2, where the plain order made every XCD stream
+// all of Wp.
 // ---------------------------------------------------------------------------
 __global__ void __launch_bounds__(kProjThreads, 1)
 proj_kernel(LayerPlan P, const uint16_t* __restrict__ xt, const uint16_t* __restrict__ wp,
@@ -167,9 +170,10 @@ proj_kernel(LayerPlan P, const uint16_t* __restrict__ xt, const uint16_t* __rest
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 2, wn = wave & 3;
   const int tiles_n = (P.features + kBN - 1) / kBN, tiles_m = (P.tokens + kBM - 1) / kBM;
-  int tm, tn;
-  {
-    const int L = blockIdx.x;
+  const int tiles = tiles_n * tiles_m;
+  // token and feature tile bases of tile L
+  auto tile_of = [&](int L, int& m0_, int& n0_) {
+    int tm, tn;
     if (tiles_m % 64 == 0) {
       const int x = L % 8, j = L / 8, per = 8 * tiles_n;
       const int grp = j / per, rr = j % per;
@@ -179,8 +183,9 @@ proj_kernel(LayerPlan P, const uint16_t* __restrict__ xt, const uint16_t* __rest
       tn = L % tiles_n;
       tm = L / tiles_n;
     }
-  }
-  const int n0 = tn * kBN, m0 = tm * kBM;
+    m0_ = tm * kBM;
+    n0_ = tn * kBN;
+  };
   const int K = P.d_model, M = P.tokens, N = P.features;
   const __amdgpu_buffer_rsrc_t rx = make_rsrc(xt, (uint32_t)((int64_t)M * K * 2));
   const __amdgpu_buffer_rsrc_t rw = make_rsrc(wp, (uint32_t)((int64_t)N * K * 2));
@@ -192,9 +197,9 @@ proj_kernel(LayerPlan P, const uint16_t* __restrict__ xt, const uint16_t* __rest
   // Steps past the last load out of range (zeros, no traffic): the loads are
   // never behind a branch, so the compiler's waits stay exact (a branch made
   // it drain every load before each commit).
-  auto issue = [&](int set, int kt) {
+  auto issue = [&](int set, int kt, int m0, int n0, bool tile_live) {
     const int k0 = kt * kBK;
-    const bool live = kt < nk;
+    const bool live = tile_live && kt < nk;
     // 32-bit offsets: tokens * d_model * 2 < 2^31 (the plan checks it), so
     // even a row up to 255 past the last token stays below 2^32
 #pragma unroll
@@ -221,14 +226,8 @@ proj_kernel(LayerPlan P, const uint16_t* __restrict__ xt, const uint16_t* __rest
     }
   };
 
-  f32x16_t acc[TM][TN];
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
 
+  f32x16_t acc[TM][TN];
   const int half = lane >> 5, l32 = lane & 31;
   auto products = [&](int buf) {
     const unsigned char* A = tile(buf, 0);
@@ -251,23 +250,40 @@ proj_kernel(LayerPlan P, const uint16_t* __restrict__ xt, const uint16_t* __rest
       }
     }
   };
+  // A workgroup owns tiles blockIdx.x, blockIdx.x + gridDim.x, ...; the
+  // first two K steps of its next tile are loaded while the current tile's
+  // epilogue writes (out of range, no traffic, after its last tile).
+  int m0, n0;
+  tile_of(blockIdx.x, m0, n0);
+  issue(0, 0, m0, n0, true);
+  issue(1, 1, m0, n0, true);
+  for (int64_t L = blockIdx.x; L < tiles; L += gridDim.x) {
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
   // Step kt's rows sit in set kt % 2 and LDS buffer kt % 2; the loop runs two
   // steps per turn so that every staging index is a constant.
-  issue(0, 0);
-  issue(1, 1);
   commit(0, 0);
   __syncthreads();
   for (int kt = 0; kt < nk; kt += 2) {
-    issue(0, kt + 2);  // set 0 is free: step kt is in LDS
+    issue(0, kt + 2, m0, n0, true);  // set 0 is free: step kt is in LDS
     products(0);
     commit(1, 1);      // zeros past the last step, never read
     __syncthreads();
     if (kt + 1 >= nk) break;
-    issue(1, kt + 3);
+    issue(1, kt + 3, m0, n0, true);
     products(1);
     commit(0, 0);
     __syncthreads();
   }
+  int m1 = 0, n1 = 0;
+  const bool has_next = L + gridDim.x < tiles;
+  tile_of((int)(has_next ? L + gridDim.x : L), m1, n1);
+  issue(0, 0, m1, n1, has_next);
+  issue(1, 1, m1, n1, has_next);
 
   // Epilogue, per 64 x 64 half of the wave's tile: through LDS as bf16 rows
   // (stride 72 elements), then each lane writes 16-byte pieces: eight
@@ -334,6 +350,10 @@ proj_kernel(LayerPlan P, const uint16_t* __restrict__ xt, const uint16_t* __rest
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   }
+  m0 = m1;
+  n0 = n1;
+  __syncthreads();  // every wave is done with the staging area before the next commit
+  }
 }
 
 }  // namespace
@@ -346,7 +366,9 @@ gbla_status launch_project(const LayerPlan& p, const void* x, const float* conv_
   if (tiles > 2147483647LL) return GBLA_ERR_UNSUPPORTED;  // the grid's x extent; nothing enqueued
   hipLaunchKernelGGL(conv_x_kernel, dim3((p.d_model + 127) / 128, (p.tokens + 16 * kConvRun - 1) / (16 * kConvRun)),
                      dim3(kThreads), 0, st, p, (const uint16_t*)x, conv_x, cu, (uint16_t*)xt);
-  const dim3 grid((unsigned)tiles);
+  // one workgroup per CU (256 on MI355X), each owning every 256th tile; a
+  // multiple of 8 keeps tile L on XCD L % 8
+  const dim3 grid((unsigned)(tiles < kProjGrid ? tiles : kProjGrid));
   hipLaunchKernelGGL(proj_kernel, grid, dim3(kProjThreads), 0, st, p, (const uint16_t*)xt,
                      (const uint16_t*)w_proj, (uint16_t*)q, (uint16_t*)k, (uint16_t*)v,
                      (uint16_t*)r, (uint16_t*)a);
