@@ -37,19 +37,29 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def algorithmic_bytes(inp, part: str) -> int:
+def algorithmic_bytes(inp, part: str, gate: bool = True, norm: bool = True) -> int:
     """Bytes each stage must move at least once (inputs read once, y written once).
     Per token and head, with e = element size of the inputs:
       state:   k, v (2 d e) + a (e)          = (2d + 1) e
       readout: q, r (2 d e) + y (4 d)        = 2 d e + 4 d
-      forward: (4d + 1) e + 4 d               (770 B at d = 64, bf16)"""
+      forward: (4d + 1) e + 4 d               (770 B at d = 64, bf16)
+    Without the key gates a is not read; without the gated norm r is not read."""
     w = inp.workload
     e = 2 if w.dtype == "bf16" else 4
     d = w.head_dim
     th = inp.tokens * w.heads
-    per = {"state": (2 * d + 1) * e, "readout": 2 * d * e + 4 * d,
-           "forward": (4 * d + 1) * e + 4 * d}[part]
+    a_b = e if gate else 0
+    r_b = d * e if norm else 0
+    per = {"state": 2 * d * e + a_b, "readout": d * e + r_b + 4 * d,
+           "forward": 3 * d * e + a_b + r_b + 4 * d}[part]
     return th * per
+
+
+# The paper's ablation rows (Section 4, "Ablation") as forward-bench options:
+# name -> (flags attribute of the binding, gate kept, conv kept, norm kept).
+SWITCHES = {"none": (None, True, True, True), "no_gate": ("NO_GATE", False, True, True),
+            "no_conv": ("NO_CONV", True, False, True), "no_norm": ("NO_NORM", True, True, False),
+            "bla": ("BLA", False, False, False)}
 
 
 def traffic_from_profiles(kernel: str, workload: str):
@@ -67,7 +77,7 @@ def traffic_from_profiles(kernel: str, workload: str):
     return rec.get("bytes_per_launch")
 
 
-def cpu_baseline(inp, seconds: float):
+def cpu_baseline(inp, seconds: float, gate: bool = True, conv: bool = True, norm: bool = True):
     import oracle
     orc = oracle.load()
     threads = orc.max_threads()
@@ -76,7 +86,7 @@ def cpu_baseline(inp, seconds: float):
     t_start = time.perf_counter()
     while True:
         t0 = time.perf_counter()
-        orc.forward_inputs(inp, want=("y",), nthreads=threads)
+        orc.forward_inputs(inp, want=("y",), nthreads=threads, gate=gate, conv=conv, norm=norm)
         times.append(time.perf_counter() - t0)
         if len(times) >= 3 and time.perf_counter() - t_start >= seconds:
             break
@@ -234,6 +244,9 @@ def main():
                     help="forward (the headline metric), the backward pass (gbla_backward) or "
                          "the full layer from the embeddings (gbla_layer_forward; --workload "
                          "layer_b8_n2048 or layer_b8_n32768)")
+    ap.add_argument("--switches", choices=tuple(SWITCHES), default="none",
+                    help="forward pass only: the ablation switches of the timed forward "
+                         "(removed inputs are not passed)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only copy 256 MiB device-to-device --steps times (reference for "
                          "rocprofv3 FETCH_SIZE / WRITE_SIZE scaling)")
@@ -279,12 +292,20 @@ def main():
         sets.append(t)
     shape = gbla.make_shape(base["q"], base["conv_w"], inp.eps, base["cu_seqlens"], base["max_seqlen"])
     ws = gbla.alloc_workspace(shape, dev)
+    flag_name, keep_gate, keep_conv, keep_norm = SWITCHES[args.switches]
+    flags = getattr(gbla, flag_name) if flag_name else 0
+
+    def used(t):
+        """a, r, taps, gamma of a set, None where a switch removes them."""
+        return (t["a"] if keep_gate else None, t["r"] if keep_norm else None,
+                t["conv_w"] if keep_conv else None, t["gamma"] if keep_norm else None)
 
     def step(i):
         t = sets[i % nsets]
-        gbla.forward(t["q"], t["k"], t["v"], t["a"], t["r"], t["conv_w"], t["gamma"], eps=inp.eps,
+        a, r, cw, gm = used(t)
+        gbla.forward(t["q"], t["k"], t["v"], a, r, cw, gm, eps=inp.eps,
                      cu_seqlens=t["cu_seqlens"], max_seqlen=t["max_seqlen"], workspace=ws,
-                     out=t["out"])
+                     out=t["out"], flags=flags)
 
     for i in range(args.warmup):
         step(i)
@@ -318,7 +339,7 @@ def main():
     # Practical ceiling: a device-to-device copy moving the forward's
     # algorithmic bytes (half read, half written), over as many rotating
     # buffers as the forward uses, timed the same way.
-    half = algorithmic_bytes(inp, "forward") // 2 // 4
+    half = algorithmic_bytes(inp, "forward", keep_gate, keep_norm) // 2 // 4
     bufs = [torch.empty(half, dtype=torch.float32, device=dev) for _ in range(nsets + 1)]
     for b in bufs:
         b.fill_(1.0)
@@ -342,24 +363,25 @@ def main():
     pairs, calls = [], []
     for i in range(n_meas):
         t = sets[i % nsets]
-        gbla.state(t["k"], t["v"], t["a"], t["conv_w"], cu_seqlens=t["cu_seqlens"],
-                   max_seqlen=t["max_seqlen"], workspace=ws)
+        a_, r_, cw_, gm_ = used(t)
+        gbla.state(t["k"], t["v"], a_, cw_, cu_seqlens=t["cu_seqlens"],
+                   max_seqlen=t["max_seqlen"], workspace=ws, flags=flags)
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         ka, kb = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         ka.record(stream)
         kb.record(stream)
         a.record(stream)
-        gbla.readout(t["q"], t["r"], t["conv_w"], t["gamma"], ws, eps=inp.eps,
+        gbla.readout(t["q"], r_, cw_, gm_, ws, eps=inp.eps,
                      cu_seqlens=t["cu_seqlens"], max_seqlen=t["max_seqlen"], out=t["out"],
-                     kernel_events=(ka, kb))
+                     kernel_events=(ka, kb), flags=flags)
         b.record(stream)
         pairs.append((ka, kb))
         calls.append((a, b))
     torch.cuda.synchronize()
     readout_ms = statistics.mean(a.elapsed_time(b) for a, b in pairs)
     readout_call_ms = statistics.mean(a.elapsed_time(b) for a, b in calls)
-    ach = algorithmic_bytes(inp, "readout") / (readout_ms * 1e-3) / 1e9
-    fwd_gbps = algorithmic_bytes(inp, "forward") / (ms_per_step * 1e-3) / 1e9
+    ach = algorithmic_bytes(inp, "readout", keep_gate, keep_norm) / (readout_ms * 1e-3) / 1e9
+    fwd_gbps = algorithmic_bytes(inp, "forward", keep_gate, keep_norm) / (ms_per_step * 1e-3) / 1e9
 
     res = {
         "metric": METRIC,
@@ -388,10 +410,13 @@ def main():
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBPS, 4),
                      "avg_launch_ms": readout_ms,
                      "avg_call_ms": readout_call_ms,
-                     "traffic": traffic_from_profiles("readout_stream_kernel", w.name)},
+                     "traffic": (traffic_from_profiles("readout_stream_kernel", w.name)
+                                 if args.switches == "none" else None)},
     }
+    if args.switches != "none":
+        res["config"]["switches"] = args.switches
     if not args.no_cpu_baseline:
-        res["cpu_baseline"] = cpu_baseline(inp, args.cpu_seconds)
+        res["cpu_baseline"] = cpu_baseline(inp, args.cpu_seconds, keep_gate, keep_conv, keep_norm)
     print(json.dumps(res), flush=True)
 
 
