@@ -226,7 +226,6 @@ proj_kernel(LayerPlan P, const uint16_t* __restrict__ xt, const uint16_t* __rest
     }
   };
 
-
   f32x16_t acc[TM][TN];
   const int half = lane >> 5, l32 = lane & 31;
   auto products = [&](int buf) {
@@ -259,100 +258,100 @@ proj_kernel(LayerPlan P, const uint16_t* __restrict__ xt, const uint16_t* __rest
   issue(1, 1, m0, n0, true);
   for (int64_t L = blockIdx.x; L < tiles; L += gridDim.x) {
 #pragma unroll
-  for (int i = 0; i < TM; ++i)
+    for (int i = 0; i < TM; ++i)
 #pragma unroll
-    for (int j = 0; j < TN; ++j)
+      for (int j = 0; j < TN; ++j)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
-  // Step kt's rows sit in set kt % 2 and LDS buffer kt % 2; the loop runs two
-  // steps per turn so that every staging index is a constant.
-  commit(0, 0);
-  __syncthreads();
-  for (int kt = 0; kt < nk; kt += 2) {
-    issue(0, kt + 2, m0, n0, true);  // set 0 is free: step kt is in LDS
-    products(0);
-    commit(1, 1);      // zeros past the last step, never read
-    __syncthreads();
-    if (kt + 1 >= nk) break;
-    issue(1, kt + 3, m0, n0, true);
-    products(1);
+        for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
+    // Step kt's rows sit in set kt % 2 and LDS buffer kt % 2; the loop runs two
+    // steps per turn so that every staging index is a constant.
     commit(0, 0);
     __syncthreads();
-  }
-  int m1 = 0, n1 = 0;
-  const bool has_next = L + gridDim.x < tiles;
-  tile_of((int)(has_next ? L + gridDim.x : L), m1, n1);
-  issue(0, 0, m1, n1, has_next);
-  issue(1, 1, m1, n1, has_next);
-
-  // Epilogue, per 64 x 64 half of the wave's tile: through LDS as bf16 rows
-  // (stride 72 elements), then each lane writes 16-byte pieces: eight
-  // consecutive features of one token, which are eight consecutive channels
-  // of one head (d is a multiple of 8).  Gate-logit features, whose
-  // destinations are H rows apart, are written one by one.
-  uint16_t* ep = reinterpret_cast<uint16_t*>(lds_raw) + wave * 64 * kEpRow;
-  const int Hd = P.heads * P.d;
-  const int piece = lane & 7;                     // eight features 8 piece .. 8 piece + 7
-  const int nb = n0 + kWaveN * wn + 8 * piece;    // first feature of the piece
-  const bool in_proj = nb + 8 <= 4 * Hd;          // else gate logits (or past N)
-  const int blk = in_proj ? nb / Hd : 0, h = in_proj ? (nb % Hd) / P.d : 0, e = in_proj ? nb % P.d : 0;
-  uint16_t* const dst = blk == 0 ? q : blk == 1 ? k : blk == 2 ? v : r;
-  // Destination rows are linear in the token within a tile when its tokens
-  // are packed rows or lie in one dense sequence: then one row index per lane
-  // (for the tile's first token) and an offset per pass, with no division.
-  const bool linear = P.ragged || P.rows % kBM == 0;
-  int64_t b0 = 0, pos0 = m0;
-  if (!P.ragged) {
-    b0 = m0 / P.rows;
-    pos0 = m0 - b0 * P.rows;
-  }
-  auto out_row = [&](int head, int m) -> int64_t {  // row of (head, token m) in [.., n, d] / [H, T, d]
-    if (P.ragged) return (int64_t)head * M + m;
-    if (linear) return (b0 * P.heads + head) * P.rows + pos0 + (m - m0);
-    const int64_t b = m / P.rows;
-    return (b * P.heads + head) * P.rows + (m - b * P.rows);
-  };
-#pragma unroll
-  for (int si = 0; si < TM / 2; ++si) {
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int j = 0; j < TN; ++j) {
-#pragma unroll
-        for (int rr = 0; rr < 16; ++rr) {
-          const int row = 32 * i + 8 * (rr >> 2) + 4 * half + (rr & 3);
-          ep[row * kEpRow + 32 * j + l32] = bf16_bits_rne(acc[2 * si + i][j][rr]);
-        }
-      }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-#pragma unroll
-    for (int pass = 0; pass < 8; ++pass) {
-      const int row = 8 * pass + (lane >> 3);
-      const int m = m0 + kWaveM * wm + 64 * si + row;
-      if (m >= M || nb >= N) continue;
-      const uint16_t* src = ep + row * kEpRow + 8 * piece;
-      if (in_proj) {
-        *reinterpret_cast<u32x4_t*>(dst + out_row(h, m) * P.d + e) = *reinterpret_cast<const u32x4_t*>(src);
-      } else {
-#pragma unroll
-        for (int f = 0; f < 8; ++f) {
-          const int n = nb + f;
-          if (n >= N) break;
-          // gate logits (every earlier feature is in a 16-byte piece)
-          a[out_row(n - 4 * Hd, m)] = src[f];
-        }
-      }
+    for (int kt = 0; kt < nk; kt += 2) {
+      issue(0, kt + 2, m0, n0, true);  // set 0 is free: step kt is in LDS
+      products(0);
+      commit(1, 1);      // zeros past the last step, never read
+      __syncthreads();
+      if (kt + 1 >= nk) break;
+      issue(1, kt + 3, m0, n0, true);
+      products(1);
+      commit(0, 0);
+      __syncthreads();
     }
-    // the next half reuses this wave's staging rows
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-  }
-  m0 = m1;
-  n0 = n1;
-  __syncthreads();  // every wave is done with the staging area before the next commit
+    int m1 = 0, n1 = 0;
+    const bool has_next = L + gridDim.x < tiles;
+    tile_of((int)(has_next ? L + gridDim.x : L), m1, n1);
+    issue(0, 0, m1, n1, has_next);
+    issue(1, 1, m1, n1, has_next);
+
+    // Epilogue, per 64 x 64 half of the wave's tile: through LDS as bf16 rows
+    // (stride 72 elements), then each lane writes 16-byte pieces: eight
+    // consecutive features of one token, which are eight consecutive channels
+    // of one head (d is a multiple of 8).  Gate-logit features, whose
+    // destinations are H rows apart, are written one by one.
+    uint16_t* ep = reinterpret_cast<uint16_t*>(lds_raw) + wave * 64 * kEpRow;
+    const int Hd = P.heads * P.d;
+    const int piece = lane & 7;                     // eight features 8 piece .. 8 piece + 7
+    const int nb = n0 + kWaveN * wn + 8 * piece;    // first feature of the piece
+    const bool in_proj = nb + 8 <= 4 * Hd;          // else gate logits (or past N)
+    const int blk = in_proj ? nb / Hd : 0, h = in_proj ? (nb % Hd) / P.d : 0, e = in_proj ? nb % P.d : 0;
+    uint16_t* const dst = blk == 0 ? q : blk == 1 ? k : blk == 2 ? v : r;
+    // Destination rows are linear in the token within a tile when its tokens
+    // are packed rows or lie in one dense sequence: then one row index per lane
+    // (for the tile's first token) and an offset per pass, with no division.
+    const bool linear = P.ragged || P.rows % kBM == 0;
+    int64_t b0 = 0, pos0 = m0;
+    if (!P.ragged) {
+      b0 = m0 / P.rows;
+      pos0 = m0 - b0 * P.rows;
+    }
+    auto out_row = [&](int head, int m) -> int64_t {  // row of (head, token m) in [.., n, d] / [H, T, d]
+      if (P.ragged) return (int64_t)head * M + m;
+      if (linear) return (b0 * P.heads + head) * P.rows + pos0 + (m - m0);
+      const int64_t b = m / P.rows;
+      return (b * P.heads + head) * P.rows + (m - b * P.rows);
+    };
+#pragma unroll
+    for (int si = 0; si < TM / 2; ++si) {
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+#pragma unroll
+          for (int rr = 0; rr < 16; ++rr) {
+            const int row = 32 * i + 8 * (rr >> 2) + 4 * half + (rr & 3);
+            ep[row * kEpRow + 32 * j + l32] = bf16_bits_rne(acc[2 * si + i][j][rr]);
+          }
+        }
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+      for (int pass = 0; pass < 8; ++pass) {
+        const int row = 8 * pass + (lane >> 3);
+        const int m = m0 + kWaveM * wm + 64 * si + row;
+        if (m >= M || nb >= N) continue;
+        const uint16_t* src = ep + row * kEpRow + 8 * piece;
+        if (in_proj) {
+          *reinterpret_cast<u32x4_t*>(dst + out_row(h, m) * P.d + e) = *reinterpret_cast<const u32x4_t*>(src);
+        } else {
+#pragma unroll
+          for (int f = 0; f < 8; ++f) {
+            const int n = nb + f;
+            if (n >= N) break;
+            // gate logits (every earlier feature is in a 16-byte piece)
+            a[out_row(n - 4 * Hd, m)] = src[f];
+          }
+        }
+      }
+      // the next half reuses this wave's staging rows
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    }
+    m0 = m1;
+    n0 = n1;
+    __syncthreads();  // every wave is done with the staging area before the next commit
   }
 }
 
