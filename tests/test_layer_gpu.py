@@ -45,6 +45,15 @@ CASES = {
                                   conv_width=1, seed=83), None),
     "ragged_dm128_h2_d64": (LW("l4", batch=4, seqlen=0, d_model=128, heads=2, head_dim=64,
                                conv_width=4, seed=84, ragged=True), [5, 0, 130, 1, 200]),
+    # more tiles than the GEMM's 256 persistent workgroups: 275 x 3 tiles in the
+    # plain order, the last token tile partial, sequences crossing tile edges
+    "ragged_dm128_h2_d64_T70351": (LW("l5", batch=5, seqlen=0, d_model=128, heads=2, head_dim=64,
+                                      conv_width=4, seed=85, ragged=True),
+                                   [30001, 17, 0, 40000, 333]),
+    # 64 x 5 tiles in the XCD-grouped order, with 128-token sequences (a tile
+    # holds two, so the scatter computes each token's sequence)
+    "dm128_h4_d64_b128_n128": (LW("l6", batch=128, seqlen=128, d_model=128, heads=4, head_dim=64,
+                                  conv_width=3, seed=86), None),
 }
 
 
