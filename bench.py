@@ -55,7 +55,7 @@ def algorithmic_bytes(inp, part: str, gate: bool = True, norm: bool = True) -> i
     return th * per
 
 
-# The paper's ablation rows (Section 4, "Ablation") as forward-bench options:
+# The paper's ablation rows (Section 3, "Ablation", Table 4) as forward-bench options:
 # name -> (flags attribute of the binding, gate kept, conv kept, norm kept).
 SWITCHES = {"none": (None, True, True, True), "no_gate": ("NO_GATE", False, True, True),
             "no_conv": ("NO_CONV", True, False, True), "no_norm": ("NO_NORM", True, True, False),

@@ -61,8 +61,8 @@ typedef enum {
 typedef enum { GBLA_F32 = 0, GBLA_BF16 = 1 } gbla_dtype;
 
 /*
- * Ablation switches, the rows of the paper's ablation table (Section 4,
- * "Ablation"; "W/o Key gating", "W/o Conv1D", "W/o Gated RMSNorm", and all
+ * Ablation switches, the rows of the paper's ablation table (Section 3,
+ * "Ablation", Table 4; "W/o Key gating", "W/o Conv1D", "W/o Gated RMSNorm", and all
  * three, which is plain bidirectional linear attention, Eq. (1)).  OR them
  * into shape->flags.  An input that a switch removes may be NULL and is
  * ignored if given.
@@ -119,6 +119,21 @@ gbla_status gbla_forward(const gbla_shape* shape, const void* q, const void* k,
                          const float* conv_w, const float* norm_w,
                          const int32_t* cu_seqlens, void* workspace,
                          size_t workspace_bytes, float* out, void* stream);
+
+/*
+ * gbla_forward, timed on the GPU: start_event and stop_event (hipEvent_t,
+ * created by the caller, either may be NULL) are recorded on the stream
+ * just before the pass's first kernel and as its last kernel ends
+ * (hipExtLaunchKernel), so hipEventElapsedTime gives the pass's time on the
+ * GPU without the launch gap that follows it.  Results, argument checks and
+ * errors are gbla_forward's.
+ */
+gbla_status gbla_forward_timed(const gbla_shape* shape, const void* q, const void* k,
+                               const void* v, const void* gate_logits, const void* out_gate,
+                               const float* conv_w, const float* norm_w,
+                               const int32_t* cu_seqlens, void* workspace,
+                               size_t workspace_bytes, float* out, void* stream,
+                               void* start_event, void* stop_event);
 
 /*
  * The Conv1D alone (Section 2.1, item "Conv1D"): writes the convolved

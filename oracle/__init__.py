@@ -111,7 +111,7 @@ class Oracle:
         """Run the oracle on a ``paper_2606_07317_amd.inputs.Inputs`` batch.
 
         ``gate``, ``conv`` and ``norm`` are the ablations of the paper's
-        ablation table (Section 4, "Ablation"), expressed through the inputs
+        ablation table (Section 3, "Ablation", Table 4), expressed through the inputs
         so that the arithmetic above is unchanged:
           gate=False  constant logits, hence uniform gates g_j = 1/n
                       (Section 2.1, key gating; the softmax of a constant);

@@ -74,10 +74,12 @@ size_t gbla_workspace_bytes(const gbla_shape* shape) {
   return dense.total_bytes > ragged.total_bytes ? dense.total_bytes : ragged.total_bytes;
 }
 
-gbla_status gbla_forward(const gbla_shape* shape, const void* q, const void* k, const void* v,
-                         const void* gate_logits, const void* out_gate, const float* conv_w,
-                         const float* norm_w, const int32_t* cu_seqlens, void* workspace,
-                         size_t workspace_bytes, float* out, void* stream) {
+static gbla_status forward_entry(const gbla_shape* shape, const void* q, const void* k,
+                                 const void* v, const void* gate_logits, const void* out_gate,
+                                 const float* conv_w, const float* norm_w,
+                                 const int32_t* cu_seqlens, void* workspace,
+                                 size_t workspace_bytes, float* out, void* stream,
+                                 gbla::KernelEvents ev) {
   Plan p;
   GBLA_TRY(gbla::make_plan(shape, cu_seqlens != nullptr, &p));
   gate_logits = unless(p, GBLA_NO_GATE, gate_logits);
@@ -90,9 +92,34 @@ gbla_status gbla_forward(const gbla_shape* shape, const void* q, const void* k, 
   if (!(p.flags & GBLA_NO_GATE)) GBLA_TRY(check_logits(p, gate_logits));
   GBLA_TRY(check_ws(p, workspace, workspace_bytes));
   hipStream_t st = static_cast<hipStream_t>(stream);
+  if (ev.start && hipEventRecord(ev.start, st) != hipSuccess) return GBLA_ERR_HIP;
   GBLA_TRY(gbla::launch_state(p, k, v, gate_logits, conv_w, cu_seqlens, workspace, nullptr,
                               nullptr, nullptr, st));
-  return gbla::launch_readout(p, q, out_gate, conv_w, norm_w, cu_seqlens, workspace, out, st);
+  gbla::KernelEvents last;
+  last.stop = ev.stop;
+  return gbla::launch_readout(p, q, out_gate, conv_w, norm_w, cu_seqlens, workspace, out, st,
+                              last);
+}
+
+gbla_status gbla_forward(const gbla_shape* shape, const void* q, const void* k, const void* v,
+                         const void* gate_logits, const void* out_gate, const float* conv_w,
+                         const float* norm_w, const int32_t* cu_seqlens, void* workspace,
+                         size_t workspace_bytes, float* out, void* stream) {
+  return forward_entry(shape, q, k, v, gate_logits, out_gate, conv_w, norm_w, cu_seqlens,
+                       workspace, workspace_bytes, out, stream, {});
+}
+
+gbla_status gbla_forward_timed(const gbla_shape* shape, const void* q, const void* k,
+                               const void* v, const void* gate_logits, const void* out_gate,
+                               const float* conv_w, const float* norm_w,
+                               const int32_t* cu_seqlens, void* workspace,
+                               size_t workspace_bytes, float* out, void* stream,
+                               void* start_event, void* stop_event) {
+  gbla::KernelEvents ev;
+  ev.start = static_cast<hipEvent_t>(start_event);
+  ev.stop = static_cast<hipEvent_t>(stop_event);
+  return forward_entry(shape, q, k, v, gate_logits, out_gate, conv_w, norm_w, cu_seqlens,
+                       workspace, workspace_bytes, out, stream, ev);
 }
 
 gbla_status gbla_conv1d(const gbla_shape* shape, const void* q, const void* k, const void* v,

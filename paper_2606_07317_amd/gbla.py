@@ -68,6 +68,8 @@ def load_library(path: str = LIB_PATH):
     lib.gbla_workspace_bytes.restype = sz
     lib.gbla_forward.argtypes = [SP, P, P, P, P, P, P, P, P, P, sz, P, P]
     lib.gbla_forward.restype = ctypes.c_int
+    lib.gbla_forward_timed.argtypes = [SP, P, P, P, P, P, P, P, P, P, sz, P, P, P, P]
+    lib.gbla_forward_timed.restype = ctypes.c_int
     lib.gbla_conv1d.argtypes = [SP, P, P, P, P, P, P, P, P, P]
     lib.gbla_conv1d.restype = ctypes.c_int
     lib.gbla_state.argtypes = [SP, P, P, P, P, P, P, sz, P, P, P]
@@ -123,6 +125,23 @@ def _check(t: torch.Tensor, name: str, dtype=None, device=None):
         raise TypeError("%s must be %s, got %s" % (name, dtype, t.dtype))
     if device is not None and t.device != device:
         raise ValueError("%s is on %s, expected %s" % (name, t.device, device))
+
+
+def _check_out(out: torch.Tensor, shape, dev, name: str = "out"):
+    """An output buffer the kernels write in full: fp32, contiguous, on the
+    device of the inputs, with exactly the expected shape."""
+    _check(out, name, torch.float32, dev)
+    if tuple(out.shape) != tuple(shape):
+        raise ValueError("%s has shape %s, expected %s" % (name, tuple(out.shape), tuple(shape)))
+
+
+def _check_ws(ws: torch.Tensor, dev, need: int, name: str = "workspace"):
+    """Caller-supplied scratch: a contiguous uint8 tensor on the inputs'
+    device, at least ``need`` bytes (the library checks the size and the
+    256-byte alignment again)."""
+    _check(ws, name, torch.uint8, dev)
+    if ws.numel() < need:
+        raise ValueError("%s holds %d bytes, %d needed" % (name, ws.numel(), need))
 
 
 def make_shape(q: torch.Tensor, conv_w: Optional[torch.Tensor], eps: float,
@@ -200,21 +219,30 @@ def _ptr(t: Optional[torch.Tensor]):
 
 def forward(q, k, v, gate_logits, out_gate, conv_w, norm_w, eps: float = 1e-6,
             cu_seqlens=None, max_seqlen=None, workspace=None, out=None, stream=None,
-            flags: int = 0) -> torch.Tensor:
+            flags: int = 0, kernel_events=None) -> torch.Tensor:
     """y = GBLA(q, k, v, a, r) on the GPU (o under NO_NORM); see include/gbla.h
-    for the layouts and the ablation switches in ``flags``."""
+    for the layouts and the ablation switches in ``flags``.
+    ``kernel_events`` = (start, stop) torch.cuda.Events recorded just before
+    the pass's first kernel and as its last kernel ends (gbla_forward_timed);
+    each must have been recorded once before, so that its HIP event exists."""
     _check_inputs(q, k, v, gate_logits, out_gate, conv_w, norm_w, cu_seqlens)
     shape = make_shape(q, conv_w, eps, cu_seqlens, max_seqlen, flags)
     if workspace is None:
         workspace = alloc_workspace(shape, q.device)
+    _check_ws(workspace, q.device, workspace_bytes(shape))
     if out is None:
         out = torch.empty(q.shape, dtype=torch.float32, device=q.device)
-    _check(out, "out", torch.float32, q.device)
-    st = load_library().gbla_forward(
-        ctypes.byref(shape), _ptr(q), _ptr(k), _ptr(v), _ptr(gate_logits), _ptr(out_gate),
-        _ptr(conv_w), _ptr(norm_w), _ptr(cu_seqlens), _ptr(workspace), workspace.numel(),
-        _ptr(out), _stream(stream))
-    _raise(st, "gbla_forward")
+    _check_out(out, q.shape, q.device)
+    args = (ctypes.byref(shape), _ptr(q), _ptr(k), _ptr(v), _ptr(gate_logits), _ptr(out_gate),
+            _ptr(conv_w), _ptr(norm_w), _ptr(cu_seqlens), _ptr(workspace), workspace.numel(),
+            _ptr(out), _stream(stream))
+    if kernel_events is None:
+        _raise(load_library().gbla_forward(*args), "gbla_forward")
+    else:
+        handles = [e.cuda_event for e in kernel_events]
+        if not all(handles):
+            raise ValueError("kernel_events must have been recorded once before")
+        _raise(load_library().gbla_forward_timed(*args, *handles), "gbla_forward_timed")
     return out
 
 
@@ -237,6 +265,7 @@ def state(k, v, gate_logits, conv_w, cu_seqlens=None, max_seqlen=None, workspace
     shape = make_shape(k, conv_w, 0.0, cu_seqlens, max_seqlen, flags)
     if workspace is None:
         workspace = alloc_workspace(shape, k.device)
+    _check_ws(workspace, k.device, workspace_bytes(shape))
     N, H, d = shape.batch, shape.heads, shape.head_dim
     S = torch.empty((N, H, d, d), dtype=torch.float32, device=k.device)
     z = torch.empty((N, H, d), dtype=torch.float32, device=k.device)
@@ -256,8 +285,10 @@ def readout(q, out_gate, conv_w, norm_w, workspace, eps: float = 1e-6, cu_seqlen
     each must have been recorded once before, so that its HIP event exists."""
     _check_inputs(q, None, None, None, out_gate, conv_w, norm_w, cu_seqlens)
     shape = make_shape(q, conv_w, eps, cu_seqlens, max_seqlen, flags)
+    _check_ws(workspace, q.device, workspace_bytes(shape))
     if out is None:
         out = torch.empty(q.shape, dtype=torch.float32, device=q.device)
+    _check_out(out, q.shape, q.device)
     args = (ctypes.byref(shape), _ptr(q), _ptr(out_gate), _ptr(conv_w), _ptr(norm_w),
             _ptr(cu_seqlens), _ptr(workspace), workspace.numel(), _ptr(out), _stream(stream))
     if kernel_events is None:
@@ -294,6 +325,7 @@ def backward(q, k, v, gate_logits, out_gate, conv_w, norm_w, dy, eps: float = 1e
     shape = make_shape(q, conv_w, eps, cu_seqlens, max_seqlen, flags)
     if workspace is None:
         workspace = torch.empty(backward_workspace_bytes(shape), dtype=torch.uint8, device=dev)
+    _check_ws(workspace, dev, backward_workspace_bytes(shape))
     f32 = dict(dtype=torch.float32, device=dev)
     want = {n: q.shape for n in ("dq", "dk", "dv")}
     if not flags & NO_NORM:
@@ -359,6 +391,7 @@ def layer_project(x, conv_x, w_proj, heads: int, head_dim: int, cu_seqlens=None,
     shape = layer_shape(x, conv_x, heads, head_dim, 0.0, cu_seqlens, max_seqlen)
     if workspace is None:
         workspace = torch.empty(layer_workspace_bytes(shape), dtype=torch.uint8, device=x.device)
+    _check_ws(workspace, x.device, layer_workspace_bytes(shape))
     if cu_seqlens is None:
         act = (shape.batch, heads, shape.seqlen, head_dim)
     else:
@@ -391,10 +424,12 @@ def layer_forward(x, conv_x, w_proj, norm_w, eps: float = 1e-6, cu_seqlens=None,
     shape = layer_shape(x, conv_x, heads, head_dim, eps, cu_seqlens, max_seqlen)
     if workspace is None:
         workspace = torch.empty(layer_workspace_bytes(shape), dtype=torch.uint8, device=x.device)
+    _check_ws(workspace, x.device, layer_workspace_bytes(shape))
+    act = ((shape.batch, heads, shape.seqlen, head_dim) if cu_seqlens is None
+           else (heads, shape.seqlen, head_dim))
     if out is None:
-        act = ((shape.batch, heads, shape.seqlen, head_dim) if cu_seqlens is None
-               else (heads, shape.seqlen, head_dim))
         out = torch.empty(act, dtype=torch.float32, device=x.device)
+    _check_out(out, act, x.device)
     st = load_library().gbla_layer_forward(
         ctypes.byref(shape), _ptr(x), _ptr(conv_x), _ptr(w_proj), _ptr(norm_w), _ptr(cu_seqlens),
         _ptr(workspace), workspace.numel(), _ptr(out), _stream(stream))

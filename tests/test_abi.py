@@ -27,7 +27,8 @@ def shape(**kw):
 def test_exports_every_declared_function(lib):
     names = gbla.declared_functions()
     assert {"gbla_forward", "gbla_workspace_bytes", "gbla_conv1d", "gbla_state",
-            "gbla_readout", "gbla_readout_timed", "gbla_status_string", "gbla_backward",
+            "gbla_readout", "gbla_readout_timed", "gbla_forward_timed", "gbla_status_string",
+            "gbla_backward",
             "gbla_backward_workspace_bytes", "gbla_layer_workspace_bytes", "gbla_layer_project",
             "gbla_layer_forward"} <= set(names)
     for n in names:

@@ -338,3 +338,55 @@ def test_gate_shift_invariance_fp32(G, dev):
     y2 = G.forward(t["q"], t["k"], t["v"], t["a"] + 3.0, t["r"], t["conv_w"], t["gamma"], eps=inp.eps)
     torch.cuda.synchronize()
     np.testing.assert_allclose(y2.cpu().numpy(), y1.cpu().numpy(), rtol=1e-5, atol=1e-5)
+
+
+def test_timed_forward_equals_forward(G, dev):
+    """gbla_forward_timed gives gbla_forward's bits, and its events bracket
+    the pass's kernels (a positive time no longer than events around the
+    call)."""
+    say("timed forward")
+    inp = inputs.make_inputs(SMALL_CASES["bf16_d64_n1000"])
+    t = inputs.device_tensors(inp, dev)
+    args = (t["q"], t["k"], t["v"], t["a"], t["r"], t["conv_w"], t["gamma"])
+    ref = G.forward(*args, eps=inp.eps)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    st = torch.cuda.current_stream()
+    for e in ev:
+        e.record(st)  # the HIP events exist from here on
+    ev[2].record(st)
+    y = G.forward(*args, eps=inp.eps, kernel_events=(ev[0], ev[1]))
+    ev[3].record(st)
+    torch.cuda.synchronize()
+    assert torch.equal(y, ref)
+    kernel_ms, call_ms = ev[0].elapsed_time(ev[1]), ev[2].elapsed_time(ev[3])
+    say("  kernels %.2f us, call %.2f us" % (1e3 * kernel_ms, 1e3 * call_ms))
+    assert 0.0 < kernel_ms <= call_ms
+
+
+def test_binding_rejects_bad_buffers(G, dev):
+    """The binding checks caller buffers before any pointer reaches the
+    library: an output of the wrong shape, dtype or device, a workspace of
+    the wrong dtype, on the host, or too small."""
+    say("binding buffer checks")
+    inp = inputs.make_inputs(SMALL_CASES["bf16_d64_n5"])
+    t = inputs.device_tensors(inp, dev)
+    args = (t["q"], t["k"], t["v"], t["a"], t["r"], t["conv_w"], t["gamma"])
+    shape = G.make_shape(t["q"], t["conv_w"], inp.eps, None, None)
+    need = G.workspace_bytes(shape)
+    bad_out = [torch.empty(t["q"].shape[:-1] + (t["q"].shape[-1] - 1,), device=dev),
+               torch.empty(t["q"].shape, dtype=torch.bfloat16, device=dev),
+               torch.empty(t["q"].shape)]
+    for out in bad_out:
+        with pytest.raises((ValueError, TypeError)):
+            G.forward(*args, eps=inp.eps, out=out)
+    bad_ws = [torch.empty(need, dtype=torch.float32, device=dev),
+              torch.empty(need, dtype=torch.uint8),
+              torch.empty(need - 1, dtype=torch.uint8, device=dev)]
+    for ws in bad_ws:
+        with pytest.raises((ValueError, TypeError)):
+            G.forward(*args, eps=inp.eps, workspace=ws)
+        with pytest.raises((ValueError, TypeError)):
+            G.state(t["k"], t["v"], t["a"], t["conv_w"], workspace=ws)
+    good = G.forward(*args, eps=inp.eps)
+    torch.cuda.synchronize()
+    assert torch.isfinite(good).all()
