@@ -274,6 +274,24 @@ gbla_status gbla_layer_forward(const gbla_layer_shape* shape, const void* x,
 /* A static, human-readable name of a status code (never NULL). */
 const char* gbla_status_string(gbla_status status);
 
+/*
+ * Measurement aid, not part of the method: one launch that moves exactly the
+ * bytes gbla_forward must move for `token_heads` (token, head) pairs of bf16
+ * inputs at head_dim d, with none of its arithmetic.  It reads q, k, v and
+ * out_gate (d bf16 each per pair, 16-byte loads) and one gate logit per pair,
+ * and writes d fp32 values per pair to out (16-byte stores): (4d + 1) * 2 +
+ * 4d bytes per pair, 770 at d = 64.  The written values are a function of
+ * the loaded bits, not GBLA.  Layouts are flat (pair-major, d contiguous).
+ * The benchmark times it beside the forward as the practical ceiling of a
+ * single pass over the same bytes.  Errors: GBLA_ERR_INVALID_ARGUMENT for a
+ * NULL pointer or negative count, GBLA_ERR_UNSUPPORTED for d not in {32, 64,
+ * 128}, GBLA_ERR_MISALIGNED unless q, k, v, out_gate, out are 16-byte and
+ * gate_logits 2-byte aligned, GBLA_ERR_HIP for a failed launch.
+ */
+gbla_status gbla_stream_ceiling(const void* q, const void* k, const void* v,
+                                const void* gate_logits, const void* out_gate,
+                                int64_t token_heads, int32_t head_dim, float* out, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

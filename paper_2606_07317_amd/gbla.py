@@ -78,6 +78,8 @@ def load_library(path: str = LIB_PATH):
     lib.gbla_readout.restype = ctypes.c_int
     lib.gbla_readout_timed.argtypes = [SP, P, P, P, P, P, P, sz, P, P, P, P]
     lib.gbla_readout_timed.restype = ctypes.c_int
+    lib.gbla_stream_ceiling.argtypes = [P, P, P, P, P, ctypes.c_int64, ctypes.c_int32, P, P]
+    lib.gbla_stream_ceiling.restype = ctypes.c_int
     lib.gbla_backward_workspace_bytes.argtypes = [SP]
     lib.gbla_backward_workspace_bytes.restype = sz
     lib.gbla_backward.argtypes = [SP, P, P, P, P, P, P, P, P, P, P, sz, P, P, P, P, P, P, P, P]
@@ -298,6 +300,29 @@ def readout(q, out_gate, conv_w, norm_w, workspace, eps: float = 1e-6, cu_seqlen
         if not all(handles):
             raise ValueError("kernel_events must have been recorded once before")
         _raise(load_library().gbla_readout_timed(*args, *handles), "gbla_readout_timed")
+    return out
+
+
+def stream_ceiling(q, k, v, gate_logits, out_gate, out=None, stream=None) -> torch.Tensor:
+    """Measurement aid (gbla_stream_ceiling): one launch that moves the
+    forward's bytes for these bf16 tensors (q, k, v, out_gate read, one logit
+    per token read, fp32 out written) with none of its arithmetic."""
+    dev = q.device
+    for t, nm in ((q, "q"), (k, "k"), (v, "v"), (out_gate, "out_gate")):
+        _check(t, nm, torch.bfloat16, dev)
+        if t.shape != q.shape:
+            raise ValueError("%s must have the shape of q" % nm)
+    _check(gate_logits, "gate_logits", torch.bfloat16, dev)
+    if gate_logits.shape != q.shape[:-1]:
+        raise ValueError("gate_logits must have shape %s" % (tuple(q.shape[:-1]),))
+    if out is None:
+        out = torch.empty(q.shape, dtype=torch.float32, device=dev)
+    _check_out(out, q.shape, dev)
+    d = q.shape[-1]
+    st = load_library().gbla_stream_ceiling(_ptr(q), _ptr(k), _ptr(v), _ptr(gate_logits),
+                                            _ptr(out_gate), q.numel() // d, d, _ptr(out),
+                                            _stream(stream))
+    _raise(st, "gbla_stream_ceiling")
     return out
 
 

@@ -212,3 +212,19 @@ def test_layer_validation(lib):
     assert proj(s, ws=None) == 4
     assert proj(s, wsb=1024) == 4
     assert proj(lshape(head_dim=16)) == 2
+
+
+def test_stream_ceiling_rejects_before_launch(lib):
+    """The measurement aid checks its arguments on the host like the entry
+    points of the method (codes of include/gbla.h); a zero count launches
+    nothing."""
+    def call(q=ALIGNED, k=ALIGNED, v=ALIGNED, a=ALIGNED, r=ALIGNED, n=1024, d=64, out=ALIGNED):
+        return lib.gbla_stream_ceiling(q, k, v, a, r, n, d, out, None)
+    assert call(q=None) == 1
+    assert call(out=None) == 1
+    assert call(n=-1) == 1
+    assert call(d=48) == 2
+    assert call(k=MIS) == 3
+    assert call(out=ALIGNED + 8) == 3
+    assert call(a=ALIGNED + 1) == 3
+    assert call(n=0) == 0

@@ -390,3 +390,28 @@ def test_binding_rejects_bad_buffers(G, dev):
     good = G.forward(*args, eps=inp.eps)
     torch.cuda.synchronize()
     assert torch.isfinite(good).all()
+
+
+@pytest.mark.parametrize("d", [32, 64, 128])
+def test_stream_ceiling_moves_every_byte(G, dev, d):
+    """gbla_stream_ceiling reads every 16-byte piece of q, k, v, r and each
+    token's logit once and writes y: its output is the XOR of the four
+    inputs' bits per 16-byte piece, plus the logit's bits on the token's
+    first 32-bit word, written twice per piece."""
+    say("stream ceiling d=%d" % d)
+    gen = torch.Generator().manual_seed(50 + d)
+    shp = (2, 3, 37, d)
+    ts = [torch.randint(-2**15, 2**15, shp, generator=gen, dtype=torch.int16) for _ in range(4)]
+    a = torch.randint(0, 2**15, shp[:-1], generator=gen, dtype=torch.int16)
+    dev_t = [t.view(torch.bfloat16).to(dev) for t in ts]
+    y = G.stream_ceiling(dev_t[0], dev_t[1], dev_t[2], a.view(torch.bfloat16).to(dev), dev_t[3])
+    torch.cuda.synchronize()
+    words = [t.numpy().view(np.uint32).reshape(-1, 4) for t in ts]  # 16-byte pieces
+    x = words[0] ^ words[1] ^ words[2] ^ words[3]
+    per_token = d // 8
+    first = np.arange(x.shape[0]) % per_token == 0
+    x = x.copy()
+    x[first, 0] += a.numpy().view(np.uint16).reshape(-1).astype(np.uint32)
+    want = np.repeat(x, 2, axis=0).reshape(-1)
+    got = y.cpu().numpy().view(np.uint32).reshape(-1)
+    assert np.array_equal(got, want)
