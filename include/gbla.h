@@ -136,6 +136,30 @@ gbla_status gbla_forward_timed(const gbla_shape* shape, const void* q, const voi
                                void* start_event, void* stop_event);
 
 /*
+ * gbla_forward for callers that cannot allocate device memory (code under
+ * graph capture, tight serving loops, harnesses that forbid allocation): no
+ * workspace argument; the scratch (partial states and readout operands)
+ * lives in a fixed array of GBLA_NOALLOC_SCRATCH_BYTES in device memory that
+ * each GPU holds from its first such call until the process ends.  Nothing
+ * is allocated or freed by this call.  Shapes whose gbla_forward scratch
+ * (the plan's size for the reading in use, dense or ragged) exceeds that
+ * size are refused with GBLA_ERR_WORKSPACE before anything is launched;
+ * about 4.5 MB serve B=1, H=8, n=32768, d=64.  The GPU is the stream's
+ * (the current device for the null stream).  Every call on one GPU uses that
+ * GPU's one array: calls that overlap in time on one GPU (different streams,
+ * or the same array captured into graphs replayed concurrently) race and
+ * must be serialised by the caller.  The array keeps the last call's
+ * contents; every call initialises what it reads.  Other arguments, results
+ * and errors are gbla_forward's; GBLA_ERR_HIP also if the array's device
+ * address cannot be looked up.
+ */
+#define GBLA_NOALLOC_SCRATCH_BYTES ((size_t)16 << 20)
+gbla_status gbla_forward_noalloc(const gbla_shape* shape, const void* q, const void* k,
+                                 const void* v, const void* gate_logits, const void* out_gate,
+                                 const float* conv_w, const float* norm_w,
+                                 const int32_t* cu_seqlens, float* out, void* stream);
+
+/*
  * The Conv1D alone (Section 2.1, item "Conv1D"): writes the convolved
  * q_t, k_t, v_t (fp32, same layout as q) of every token.  Test hook; the
  * forward pass fuses the conv into its loads and never writes these.

@@ -13,7 +13,8 @@ LIB = os.path.join(PKG, "libgbla.so")
 SOURCES = [os.path.join(CSRC, "gbla_kernels.hip"), os.path.join(CSRC, "gbla_stream.hip"),
            os.path.join(CSRC, "gbla_backward.hip"), os.path.join(CSRC, "gbla_layer.hip"),
            os.path.join(CSRC, "gbla_plan.cpp"), os.path.join(CSRC, "gbla_ext_plan.cpp"),
-           os.path.join(CSRC, "gbla_api.cpp"), os.path.join(CSRC, "gbla_ceiling.hip")]
+           os.path.join(CSRC, "gbla_api.cpp"), os.path.join(CSRC, "gbla_ceiling.hip"),
+           os.path.join(CSRC, "gbla_noalloc.hip")]
 
 # Packed fp32 VALU ops are switched off for all device code; hipcc's host
 # pass warns that it does not know the feature, which is harmless.

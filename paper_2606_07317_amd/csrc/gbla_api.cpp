@@ -63,23 +63,13 @@ gbla_status check_used(std::initializer_list<const void*> used) {
 
 }  // namespace
 
-extern "C" {
 
-size_t gbla_workspace_bytes(const gbla_shape* shape) {
-  // The shape alone does not say whether cu_seqlens will be given, so the
-  // size covers both readings (dense: B*n tokens, ragged: T = seqlen tokens).
-  Plan dense, ragged;
-  if (gbla::make_plan(shape, false, &dense) != GBLA_OK) return 0;
-  if (gbla::make_plan(shape, true, &ragged) != GBLA_OK) return 0;
-  return dense.total_bytes > ragged.total_bytes ? dense.total_bytes : ragged.total_bytes;
-}
+namespace gbla {
 
-static gbla_status forward_entry(const gbla_shape* shape, const void* q, const void* k,
-                                 const void* v, const void* gate_logits, const void* out_gate,
-                                 const float* conv_w, const float* norm_w,
-                                 const int32_t* cu_seqlens, void* workspace,
-                                 size_t workspace_bytes, float* out, void* stream,
-                                 gbla::KernelEvents ev) {
+gbla_status forward_entry(const gbla_shape* shape, const void* q, const void* k, const void* v,
+                          const void* gate_logits, const void* out_gate, const float* conv_w,
+                          const float* norm_w, const int32_t* cu_seqlens, void* workspace,
+                          size_t workspace_bytes, float* out, void* stream, KernelEvents ev) {
   Plan p;
   GBLA_TRY(gbla::make_plan(shape, cu_seqlens != nullptr, &p));
   gate_logits = unless(p, GBLA_NO_GATE, gate_logits);
@@ -101,12 +91,26 @@ static gbla_status forward_entry(const gbla_shape* shape, const void* q, const v
                               last);
 }
 
+}  // namespace gbla
+
+extern "C" {
+
+size_t gbla_workspace_bytes(const gbla_shape* shape) {
+  // The shape alone does not say whether cu_seqlens will be given, so the
+  // size covers both readings (dense: B*n tokens, ragged: T = seqlen tokens).
+  Plan dense, ragged;
+  if (gbla::make_plan(shape, false, &dense) != GBLA_OK) return 0;
+  if (gbla::make_plan(shape, true, &ragged) != GBLA_OK) return 0;
+  return dense.total_bytes > ragged.total_bytes ? dense.total_bytes : ragged.total_bytes;
+}
+
+
 gbla_status gbla_forward(const gbla_shape* shape, const void* q, const void* k, const void* v,
                          const void* gate_logits, const void* out_gate, const float* conv_w,
                          const float* norm_w, const int32_t* cu_seqlens, void* workspace,
                          size_t workspace_bytes, float* out, void* stream) {
-  return forward_entry(shape, q, k, v, gate_logits, out_gate, conv_w, norm_w, cu_seqlens,
-                       workspace, workspace_bytes, out, stream, {});
+  return gbla::forward_entry(shape, q, k, v, gate_logits, out_gate, conv_w, norm_w, cu_seqlens,
+                             workspace, workspace_bytes, out, stream, {});
 }
 
 gbla_status gbla_forward_timed(const gbla_shape* shape, const void* q, const void* k,
@@ -118,8 +122,8 @@ gbla_status gbla_forward_timed(const gbla_shape* shape, const void* q, const voi
   gbla::KernelEvents ev;
   ev.start = static_cast<hipEvent_t>(start_event);
   ev.stop = static_cast<hipEvent_t>(stop_event);
-  return forward_entry(shape, q, k, v, gate_logits, out_gate, conv_w, norm_w, cu_seqlens,
-                       workspace, workspace_bytes, out, stream, ev);
+  return gbla::forward_entry(shape, q, k, v, gate_logits, out_gate, conv_w, norm_w, cu_seqlens,
+                             workspace, workspace_bytes, out, stream, ev);
 }
 
 gbla_status gbla_conv1d(const gbla_shape* shape, const void* q, const void* k, const void* v,

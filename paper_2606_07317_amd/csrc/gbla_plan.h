@@ -63,6 +63,13 @@ struct KernelEvents {
   bool any() const { return start != nullptr || stop != nullptr; }
 };
 
+// The forward pass behind gbla_forward, gbla_forward_timed and
+// gbla_forward_noalloc (gbla_api.cpp): checks, then the kernels.
+gbla_status forward_entry(const gbla_shape* shape, const void* q, const void* k, const void* v,
+                          const void* gate_logits, const void* out_gate, const float* conv_w,
+                          const float* norm_w, const int32_t* cu_seqlens, void* workspace,
+                          size_t workspace_bytes, float* out, void* stream, KernelEvents ev);
+
 // Kernel launchers (gbla_kernels.hip).  Arguments were validated by the
 // caller; these only enqueue work on `stream`.
 gbla_status launch_conv(const Plan& p, const void* q, const void* k, const void* v,

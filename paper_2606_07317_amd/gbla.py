@@ -78,6 +78,8 @@ def load_library(path: str = LIB_PATH):
     lib.gbla_readout.restype = ctypes.c_int
     lib.gbla_readout_timed.argtypes = [SP, P, P, P, P, P, P, sz, P, P, P, P]
     lib.gbla_readout_timed.restype = ctypes.c_int
+    lib.gbla_forward_noalloc.argtypes = [SP, P, P, P, P, P, P, P, P, P, P]
+    lib.gbla_forward_noalloc.restype = ctypes.c_int
     lib.gbla_stream_ceiling.argtypes = [P, P, P, P, P, ctypes.c_int64, ctypes.c_int32, P, P]
     lib.gbla_stream_ceiling.restype = ctypes.c_int
     lib.gbla_backward_workspace_bytes.argtypes = [SP]
@@ -245,6 +247,27 @@ def forward(q, k, v, gate_logits, out_gate, conv_w, norm_w, eps: float = 1e-6,
         if not all(handles):
             raise ValueError("kernel_events must have been recorded once before")
         _raise(load_library().gbla_forward_timed(*args, *handles), "gbla_forward_timed")
+    return out
+
+
+NOALLOC_SCRATCH_BYTES = 16 << 20  # GBLA_NOALLOC_SCRATCH_BYTES
+
+
+def forward_noalloc(q, k, v, gate_logits, out_gate, conv_w, norm_w, eps: float = 1e-6,
+                    cu_seqlens=None, max_seqlen=None, out=None, stream=None,
+                    flags: int = 0) -> torch.Tensor:
+    """gbla_forward_noalloc: the forward with the library's fixed device
+    scratch instead of a workspace (for callers that cannot allocate; give
+    ``out`` to allocate nothing here either)."""
+    _check_inputs(q, k, v, gate_logits, out_gate, conv_w, norm_w, cu_seqlens)
+    shape = make_shape(q, conv_w, eps, cu_seqlens, max_seqlen, flags)
+    if out is None:
+        out = torch.empty(q.shape, dtype=torch.float32, device=q.device)
+    _check_out(out, q.shape, q.device)
+    st = load_library().gbla_forward_noalloc(
+        ctypes.byref(shape), _ptr(q), _ptr(k), _ptr(v), _ptr(gate_logits), _ptr(out_gate),
+        _ptr(conv_w), _ptr(norm_w), _ptr(cu_seqlens), _ptr(out), _stream(stream))
+    _raise(st, "gbla_forward_noalloc")
     return out
 
 

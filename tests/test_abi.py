@@ -228,3 +228,16 @@ def test_stream_ceiling_rejects_before_launch(lib):
     assert call(out=ALIGNED + 8) == 3
     assert call(a=ALIGNED + 1) == 3
     assert call(n=0) == 0
+
+
+def test_noalloc_refuses_shapes_beyond_its_scratch(lib):
+    """gbla_forward_noalloc checks the shape, then refuses any whose scratch
+    exceeds GBLA_NOALLOC_SCRATCH_BYTES, before any HIP call (so these run
+    without a GPU)."""
+    big = shape(batch=16, heads=16, seqlen=32768)  # far above 16 MiB of partials
+    assert lib.gbla_workspace_bytes(ctypes.byref(big)) > gbla.NOALLOC_SCRATCH_BYTES
+    args = [ALIGNED] * 7 + [None, ALIGNED, None]  # q..norm_w, cu_seqlens, out, stream
+    assert lib.gbla_forward_noalloc(ctypes.byref(big), *args) == 4
+    assert lib.gbla_forward_noalloc(ctypes.byref(shape(head_dim=96)), *args) == 2
+    assert lib.gbla_forward_noalloc(ctypes.byref(shape(eps=-1.0)), *args) == 1
+    assert lib.gbla_forward_noalloc(None, *args) == 1
