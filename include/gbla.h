@@ -94,8 +94,9 @@ typedef struct {
 
 /*
  * Bytes of device scratch that gbla_forward / gbla_state need for this
- * shape, for both the dense and the ragged layout.  Pure host arithmetic;
- * returns 0 for an invalid shape.  The caller allocates it once (any
+ * shape: the larger of the dense and the ragged reading, taking only a
+ * reading the entry points accept.  Pure host arithmetic; returns 0 when the
+ * shape is invalid in both readings.  The caller allocates it once (any
  * contents): the entry points initialise what they use on every call.
  */
 size_t gbla_workspace_bytes(const gbla_shape* shape);
@@ -207,8 +208,8 @@ gbla_status gbla_readout_timed(const gbla_shape* shape, const void* q, const voi
                                void* start_event, void* stop_event);
 
 /*
- * Bytes of device scratch that gbla_backward needs for this shape (dense or
- * ragged); 0 for an invalid shape.  About 12 * tokens * H * d bytes (fp32
+ * Bytes of device scratch that gbla_backward needs for this shape (the
+ * larger of the accepted dense and ragged readings; 0 if neither is).  About 12 * tokens * H * d bytes (fp32
  * gradients of the convolved q, k, v) plus per-chunk partials.
  */
 size_t gbla_backward_workspace_bytes(const gbla_shape* shape);
@@ -265,7 +266,8 @@ typedef struct {
 } gbla_layer_shape;
 
 /* Scratch bytes of gbla_layer_forward (the projections and the core's
- * workspace), for both the dense and the ragged reading; 0 if invalid. */
+ * workspace): the larger of the accepted dense and ragged readings; 0 if
+ * neither is accepted. */
 size_t gbla_layer_workspace_bytes(const gbla_layer_shape* shape);
 
 /*

@@ -139,11 +139,19 @@ _default: Optional[Oracle] = None
 
 
 def load(path: Optional[str] = None) -> Oracle:
-    """Load the oracle library, compiling it first if it is missing or stale."""
+    """Load the oracle library, compiling it first if it is missing or stale.
+
+    ``GBLA_ORACLE_LIB`` in the environment names another build of the same
+    source to load instead (the sanitizer test runs the pins on one built
+    with AddressSanitizer and UBSan)."""
     global _default
     if path is not None:
         return Oracle(path)
     if _default is None:
-        build(force=False)
-        _default = Oracle(_LIB)
+        alt = os.environ.get("GBLA_ORACLE_LIB")
+        if alt:
+            _default = Oracle(alt)
+        else:
+            build(force=False)
+            _default = Oracle(_LIB)
     return _default

@@ -97,11 +97,15 @@ extern "C" {
 
 size_t gbla_workspace_bytes(const gbla_shape* shape) {
   // The shape alone does not say whether cu_seqlens will be given, so the
-  // size covers both readings (dense: B*n tokens, ragged: T = seqlen tokens).
-  Plan dense, ragged;
-  if (gbla::make_plan(shape, false, &dense) != GBLA_OK) return 0;
-  if (gbla::make_plan(shape, true, &ragged) != GBLA_OK) return 0;
-  return dense.total_bytes > ragged.total_bytes ? dense.total_bytes : ragged.total_bytes;
+  // size covers both readings (dense: B*n tokens, ragged: T = seqlen tokens)
+  // -- each one the library accepts; 0 only when it accepts neither.
+  size_t most = 0;
+  for (int ragged = 0; ragged < 2; ++ragged) {
+    Plan p;
+    if (gbla::make_plan(shape, ragged != 0, &p) == GBLA_OK && p.total_bytes > most)
+      most = p.total_bytes;
+  }
+  return most;
 }
 
 
@@ -192,14 +196,16 @@ gbla_status gbla_readout_timed(const gbla_shape* shape, const void* q, const voi
 }
 
 size_t gbla_backward_workspace_bytes(const gbla_shape* shape) {
-  Plan dense, ragged, bd, br;
-  if (gbla::make_plan(shape, false, &dense) != GBLA_OK) return 0;
-  if (gbla::make_plan(shape, true, &ragged) != GBLA_OK) return 0;
-  if (gbla::backward_plan(dense, &bd) != GBLA_OK) return 0;
-  if (gbla::backward_plan(ragged, &br) != GBLA_OK) return 0;
-  const size_t a = gbla::make_bwd_layout(bd).total_bytes;
-  const size_t b = gbla::make_bwd_layout(br).total_bytes;
-  return a > b ? a : b;
+  // as gbla_workspace_bytes: the larger of the accepted readings
+  size_t most = 0;
+  for (int ragged = 0; ragged < 2; ++ragged) {
+    Plan p0, p;
+    if (gbla::make_plan(shape, ragged != 0, &p0) != GBLA_OK) continue;
+    if (gbla::backward_plan(p0, &p) != GBLA_OK) continue;
+    const size_t bytes = gbla::make_bwd_layout(p).total_bytes;
+    if (bytes > most) most = bytes;
+  }
+  return most;
 }
 
 gbla_status gbla_backward(const gbla_shape* shape, const void* q, const void* k, const void* v,
@@ -238,10 +244,14 @@ gbla_status gbla_backward(const gbla_shape* shape, const void* q, const void* k,
 }
 
 size_t gbla_layer_workspace_bytes(const gbla_layer_shape* shape) {
-  gbla::LayerPlan dense, ragged;
-  if (gbla::make_layer_plan(shape, false, &dense) != GBLA_OK) return 0;
-  if (gbla::make_layer_plan(shape, true, &ragged) != GBLA_OK) return 0;
-  return dense.total_bytes > ragged.total_bytes ? dense.total_bytes : ragged.total_bytes;
+  // as gbla_workspace_bytes: the larger of the accepted readings
+  size_t most = 0;
+  for (int ragged = 0; ragged < 2; ++ragged) {
+    gbla::LayerPlan L;
+    if (gbla::make_layer_plan(shape, ragged != 0, &L) == GBLA_OK && L.total_bytes > most)
+      most = L.total_bytes;
+  }
+  return most;
 }
 
 gbla_status gbla_layer_project(const gbla_layer_shape* shape, const void* x, const float* conv_x,
