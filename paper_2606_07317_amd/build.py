@@ -11,6 +11,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libgbla.so")
 SOURCES = [os.path.join(CSRC, "gbla_kernels.hip"), os.path.join(CSRC, "gbla_stream.hip"),
+           os.path.join(CSRC, "gbla_state128.hip"),
            os.path.join(CSRC, "gbla_backward.hip"), os.path.join(CSRC, "gbla_layer.hip"),
            os.path.join(CSRC, "gbla_plan.cpp"), os.path.join(CSRC, "gbla_ext_plan.cpp"),
            os.path.join(CSRC, "gbla_api.cpp"), os.path.join(CSRC, "gbla_ceiling.hip"),

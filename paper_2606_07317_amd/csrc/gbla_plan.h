@@ -89,11 +89,15 @@ gbla_status launch_readout(const Plan& p, const void* q, const void* r, const fl
 gbla_status launch_combine_f32(const Plan& p, const int32_t* cu, const float* partials,
                                float* S, float* z, float* mz, hipStream_t stream);
 
-// Streaming kernels (gbla_stream.hip): bf16 inputs, head dim 32 or 64.
+// Streaming kernels (gbla_stream.hip): bf16 inputs, head dim 32, 64 or 128.
 bool stream_supported(const Plan& p);
 gbla_status launch_state_stream(const Plan& p, const void* k, const void* v, const void* a,
                                 const float* conv_w, const int32_t* cu, float* partials,
                                 hipStream_t stream);
+// Head dim 128 (gbla_state128.hip): same partial records as launch_state_stream.
+gbla_status launch_state128(const Plan& p, const void* k, const void* v, const void* a,
+                            const float* conv_w, const int32_t* cu, float* partials,
+                            hipStream_t stream);
 gbla_status launch_readout_stream(const Plan& p, const void* q, const void* r, const float* conv_w,
                                   const float* gamma, const int32_t* cu, const unsigned char* frags,
                                   float* out, hipStream_t stream, KernelEvents ev = {});

@@ -690,10 +690,8 @@ gbla_status launch_state_stream(const Plan& p, const void* k, const void* v, con
                                 const float* conv_w, const int32_t* cu, float* partials,
                                 hipStream_t st) {
   const dim3 grid(p.units, p.heads);
-  if (p.d == 128)
-    hipLaunchKernelGGL((state_stream_kernel<128>), grid, dim3(SS<128>::kNT), 0, st, p,
-                       (const uint16_t*)k, (const uint16_t*)v, (const uint16_t*)a, conv_w, cu, partials);
-  else if (p.d == 64)
+  if (p.d == 128) return launch_state128(p, k, v, a, conv_w, cu, partials, st);
+  if (p.d == 64)
     hipLaunchKernelGGL((state_stream_kernel<64>), grid, dim3(SS<64>::kNT), 0, st, p,
                        (const uint16_t*)k, (const uint16_t*)v, (const uint16_t*)a, conv_w, cu, partials);
   else
