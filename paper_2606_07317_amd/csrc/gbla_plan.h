@@ -94,6 +94,10 @@ bool stream_supported(const Plan& p);
 gbla_status launch_state_stream(const Plan& p, const void* k, const void* v, const void* a,
                                 const float* conv_w, const int32_t* cu, float* partials,
                                 hipStream_t stream);
+// Head dim 64 (gbla_state64.hip): same partial records as launch_state_stream.
+gbla_status launch_state64(const Plan& p, const void* k, const void* v, const void* a,
+                           const float* conv_w, const int32_t* cu, float* partials,
+                           hipStream_t stream);
 // Head dim 128 (gbla_state128.hip): same partial records as launch_state_stream.
 gbla_status launch_state128(const Plan& p, const void* k, const void* v, const void* a,
                             const float* conv_w, const int32_t* cu, float* partials,

@@ -691,11 +691,8 @@ gbla_status launch_state_stream(const Plan& p, const void* k, const void* v, con
                                 hipStream_t st) {
   const dim3 grid(p.units, p.heads);
   if (p.d == 128) return launch_state128(p, k, v, a, conv_w, cu, partials, st);
-  if (p.d == 64)
-    hipLaunchKernelGGL((state_stream_kernel<64>), grid, dim3(SS<64>::kNT), 0, st, p,
-                       (const uint16_t*)k, (const uint16_t*)v, (const uint16_t*)a, conv_w, cu, partials);
-  else
-    hipLaunchKernelGGL((state_stream_kernel<32>), grid, dim3(SS<32>::kNT), 0, st, p,
+  if (p.d == 64) return launch_state64(p, k, v, a, conv_w, cu, partials, st);
+  hipLaunchKernelGGL((state_stream_kernel<32>), grid, dim3(SS<32>::kNT), 0, st, p,
                        (const uint16_t*)k, (const uint16_t*)v, (const uint16_t*)a, conv_w, cu, partials);
   return hipGetLastError() == hipSuccess ? GBLA_OK : GBLA_ERR_HIP;
 }
