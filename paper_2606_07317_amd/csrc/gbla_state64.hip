@@ -125,11 +125,13 @@ __device__ __forceinline__ void wait_vm() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x0F70);
 }
 
-__device__ __forceinline__ void ring_sync() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-  __builtin_amdgcn_s_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
-}
+// The barrier of a step, with no fence.  Only the loads into LDS write the
+// ring, and each wave has waited (vmcnt) for its own loads of the slot read
+// next before it arrives, so after the barrier that slot is complete.  A
+// workgroup fence here would make every wave wait for all of its loads in
+// flight, the later steps' too, which ends the prefetch.  The clobber keeps
+// the compiler from moving LDS accesses across the barrier.
+__device__ __forceinline__ void ring_sync() { asm volatile("s_barrier" ::: "memory"); }
 
 // Keeps the compiler from hoisting address arithmetic on x out of a step
 // (one add per read is cheaper than eight slots' worth of live addresses).
