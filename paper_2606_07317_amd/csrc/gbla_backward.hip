@@ -613,7 +613,7 @@ bwd_param_kernel(Plan P, const int32_t* __restrict__ cu, const float* __restrict
 }
 
 // ===========================================================================
-// Matrix-core path (head dim 32 or 64).
+// Matrix-core path (every head dim; at d = 128 one workgroup per CU).
 //
 // Every contraction runs on v_mfma_f32_16x16x4_f32: fp32 operands, exact
 // products, fp32 accumulation, so the results carry fp32 rounding only (the
@@ -697,6 +697,23 @@ __device__ __forceinline__ void build_frags(const float* __restrict__ src, f32x4
 #pragma unroll
     for (int i = 0; i < 4; ++i)
       v[i] = kTrans ? src[(size_t)(k0 + i) * D + row] : src[(size_t)row * D + k0 + i];
+    frag[idx] = v;
+  }
+}
+
+// The fragments of build_frags<D, false> for S' = S - z m^T: X[row][k] =
+// src[row * D + k] - zv[row] mv[k] (zv, mv in LDS).
+template <int D>
+__device__ __forceinline__ void build_frags_centred(const float* __restrict__ src, const float* zv,
+                                                    const float* mv, f32x4_t* frag) {
+  constexpr int NMB = D / 16;
+  for (int idx = threadIdx.x; idx < NMB * NMB * 64; idx += kThreads) {
+    const int f = idx >> 6, l = idx & 63;
+    const int mb = f / NMB, kq = f % NMB;
+    const int row = 16 * mb + (l & 15), k0 = 16 * kq + 4 * (l >> 4);
+    f32x4_t v;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) v[i] = fmaf(-zv[row], mv[k0 + i], src[(size_t)row * D + k0 + i]);
     frag[idx] = v;
   }
 }
@@ -905,7 +922,7 @@ __device__ __forceinline__ void reduce_sigma(const float (*v)[4], float (*red)[D
 // State, matrix-core version: the record [S_p | z_p | m_p | l_p] of a unit.
 // ---------------------------------------------------------------------------
 template <typename T, int D>
-__global__ void __launch_bounds__(kThreads, 2)
+__global__ void __launch_bounds__(kThreads, D >= 128 ? 1 : 2)
 bwd_state_mfma_kernel(Plan P, const T* __restrict__ kin, const T* __restrict__ vin,
                       const T* __restrict__ ain, const float* __restrict__ conv_w,
                       const int32_t* __restrict__ cu, float* __restrict__ partials) {
@@ -1002,23 +1019,27 @@ bwd_state_mfma_kernel(Plan P, const T* __restrict__ kin, const T* __restrict__ v
 // ---------------------------------------------------------------------------
 // Query pass, matrix-core version.
 // ---------------------------------------------------------------------------
-template <typename T, int D, bool kNorm>
-__global__ void __launch_bounds__(kThreads, 2)
+// kDS: the unit's dS partial is summed here (d <= 64).  At d = 128 the
+// token-sum accumulators and the two d x d operand layouts do not fit one
+// CU together, so this kernel writes dnum (to dnum_out, the layout of dy)
+// and bwd_dsum_mfma_kernel forms dS from it.
+template <typename T, int D, bool kNorm, bool kDS>
+__global__ void __launch_bounds__(kThreads, D >= 128 ? 1 : 2)
 bwd_query_mfma_kernel(Plan P, const T* __restrict__ qin, const T* __restrict__ rin,
                       const float* __restrict__ dy, const float* __restrict__ conv_w,
                       const float* __restrict__ gamma, const int32_t* __restrict__ cu,
                       const float* __restrict__ Sg, const float* __restrict__ zg,
                       float* __restrict__ dqt, float* __restrict__ dr, float* __restrict__ dsp,
-                      float* __restrict__ dgp) {
+                      float* __restrict__ dgp, float* __restrict__ dnum_out) {
   using C = MF<D>;
   constexpr int NMB = C::NMB;
   __shared__ f32x4_t a1[NMB * NMB * 64];  // num: A[e][c] = S[c][e]
   __shared__ f32x4_t a2[NMB * NMB * 64];  // dQh: A[c][e] = S[c][e]
-  __shared__ __attribute__((aligned(16))) float stg[4][2][C::kStage];  // [wave][Qh or dnum]
+  __shared__ __attribute__((aligned(16))) float stg[4][2][kDS ? C::kStage : 4];  // [wave][Qh or dnum]
   __shared__ f32x4_t tq[D];
-  __shared__ __attribute__((aligned(16))) float zs[D], gs[D];
+  __shared__ __attribute__((aligned(16))) float zs[D], gs[D], ms[D];
   __shared__ float red[4][D];
-  static_assert(sizeof(stg) >= D * D * sizeof(float), "staging holds a d x d matrix");
+  static_assert(!kDS || sizeof(stg) >= D * D * sizeof(float), "staging holds a d x d matrix");
   const int tid = threadIdx.x, lane = tid & 63, n = lane & 15, g = lane >> 4;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int h = blockIdx.y, unit = blockIdx.x;
@@ -1031,7 +1052,7 @@ bwd_query_mfma_kernel(Plan P, const T* __restrict__ qin, const T* __restrict__ r
   const size_t sh = (size_t)s * P.heads + h;
   const float* z = zg + sh * D;
   float* sbuf = &stg[0][0][0];
-  stage_matrix<D>(Sg + sh * D * D, sbuf);
+  if constexpr (kDS) stage_matrix<D>(Sg + sh * D * D, sbuf);
   if (tid < D) {
     float w4[4];
     load_taps4(conv_w, P.heads, h, 0, D, P.W, tid, w4);
@@ -1048,11 +1069,28 @@ bwd_query_mfma_kernel(Plan P, const T* __restrict__ qin, const T* __restrict__ r
       dgacc[kq][i] = 0.0f;
     }
   __syncthreads();
-  build_frags<D, true>(sbuf, a1);
-  build_frags<D, false>(sbuf, a2);
-  f32x4_t acc3[C::kBlocks];
+  // dQh = S dnum + z dden is formed as S' dnum + z (dden + m . dnum) with
+  // S' = S - z m^T, m = (sum_c S[c][.]) / (sum_c z[c]) (the gate-weighted
+  // mean value row): the same quantity, but without the cancellation
+  // between the two terms when the value rows share a mean (then
+  // S dnum ~ z (m . dnum) and o ~ m, and the no-norm dden + m . dnum is
+  // formed as -((o - m) . dy) / den directly).
+  const float* Ssrc = kDS ? sbuf : Sg + sh * D * D;
+  if (tid < D) {
+    float cs = 0.0f, zsum = 0.0f;
+    for (int c = 0; c < D; ++c) {
+      cs += Ssrc[(size_t)c * D + tid];
+      zsum += zs[c];
+    }
+    ms[tid] = zsum > 0.0f ? cs / zsum : 0.0f;
+  }
+  __syncthreads();
+  // the operand layouts, from the staged S, or at d = 128 straight from memory
+  build_frags<D, true>(Ssrc, a1);
+  build_frags_centred<D>(Ssrc, zs, ms, a2);
+  f32x4_t acc3[kDS ? C::kBlocks : 1];
 #pragma unroll
-  for (int k = 0; k < C::kBlocks; ++k) acc3[k] = (f32x4_t){0.0f, 0.0f, 0.0f, 0.0f};
+  for (int k = 0; k < (kDS ? C::kBlocks : 1); ++k) acc3[k] = (f32x4_t){0.0f, 0.0f, 0.0f, 0.0f};
 
   const uint32_t rows = (uint32_t)len * D;
   const __amdgpu_buffer_rsrc_t rq = make_rsrc(qin + base_row * D, rows * sizeof(T));
@@ -1063,6 +1101,8 @@ bwd_query_mfma_kernel(Plan P, const T* __restrict__ qin, const T* __restrict__ r
   const __amdgpu_buffer_rsrc_t rdq = make_rsrc(dqt + base_row * D, rows * 4u);
   const __amdgpu_buffer_rsrc_t rdr =
       kNorm ? make_rsrc(dr + base_row * D, rows * 4u) : make_rsrc(dqt, 0u);
+  const __amdgpu_buffer_rsrc_t rdn =
+      kDS ? make_rsrc(dqt, 0u) : make_rsrc(dnum_out + base_row * D, rows * 4u);
   float* X = stg[wave][0];
   float* Y = stg[wave][1];
   __syncthreads();  // fragments built; the staging area is free again
@@ -1122,7 +1162,7 @@ bwd_query_mfma_kernel(Plan P, const T* __restrict__ qin, const T* __restrict__ r
         o[kq][i] = acc1[kq][i] * inv_den;
         ss = fmaf(o[kq][i], o[kq][i], ss);
       }
-    float dnum[NMB][4], dden;
+    float dnum[NMB][4], dden, dcen;  // dcen = dden + m . dnum
     if constexpr (kNorm) {
       const float rs = 1.0f / sqrtf(sum_groups(ss) / D + P.eps);
       // gated RMSNorm backward
@@ -1153,18 +1193,30 @@ bwd_query_mfma_kernel(Plan P, const T* __restrict__ qin, const T* __restrict__ r
       // the RMSNorm leaves almost nothing along o, and summing do . o would
       // return mostly the rounding of its terms.
       dden = -P.eps * rs * rs * rs * s1 * inv_den;
-    } else {  // y = o: do = dy
-      float s2 = 0.0f;
+      float md = 0.0f;
 #pragma unroll
-      for (int kq = 0; kq < NMB; ++kq)
+      for (int kq = 0; kq < NMB; ++kq) {
+        const f32x4_t mr = *reinterpret_cast<const f32x4_t*>(&ms[16 * kq + 4 * g]);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) md = fmaf(mr[i], dnum[kq][i], md);
+      }
+      dcen = dden + sum_groups(md);
+    } else {  // y = o: do = dy
+      float s2 = 0.0f, s2c = 0.0f;
+#pragma unroll
+      for (int kq = 0; kq < NMB; ++kq) {
+        const f32x4_t mr = *reinterpret_cast<const f32x4_t*>(&ms[16 * kq + 4 * g]);
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           dnum[kq][i] = dyv[kq][i] * inv_den;
           s2 = fmaf(dyv[kq][i], o[kq][i], s2);
+          s2c = fmaf(dyv[kq][i], o[kq][i] - mr[i], s2c);
         }
+      }
       dden = -sum_groups(s2) * inv_den;
+      dcen = -sum_groups(s2c) * inv_den;
     }
-    // dQh = S dnum + z dden
+    // dQh = S' dnum + z (dden + m . dnum)
     f32x4_t acc2[NMB];
 #pragma unroll
     for (int mb = 0; mb < NMB; ++mb) acc2[mb] = (f32x4_t){0.0f, 0.0f, 0.0f, 0.0f};
@@ -1176,24 +1228,107 @@ bwd_query_mfma_kernel(Plan P, const T* __restrict__ qin, const T* __restrict__ r
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         // phi'(u) = 1 for u > 0 and e^u = phi(u) <= 1 otherwise: min(phi(u), 1)
-        dq[i] = fmaf(zr[i], dden, acc2[kq][i]) * fminf(qh[kq][i], 1.0f);
+        dq[i] = fmaf(zr[i], dcen, acc2[kq][i]) * fminf(qh[kq][i], 1.0f);
         dzacc[kq][i] = fmaf(qh[kq][i], dden, dzacc[kq][i]);
       }
       store4(rdq, eoff<D>(cur, 16 * kq + 4 * g), dq);
     }
-    // dS += sum over the block's tokens of Qh dnum^T
-    wave_lds_sync();  // the previous block's reads of X, Y are done
-    stage_sigma<D>(X, n, g, qh);
-    stage_sigma<D>(Y, n, g, dnum);
-    wave_lds_sync();
-    token_product<D>(X, Y, lane, acc3);
+    if constexpr (kDS) {
+      // dS += sum over the block's tokens of Qh dnum^T
+      wave_lds_sync();  // the previous block's reads of X, Y are done
+      stage_sigma<D>(X, n, g, qh);
+      stage_sigma<D>(Y, n, g, dnum);
+      wave_lds_sync();
+      token_product<D>(X, Y, lane, acc3);
+    } else {
+#pragma unroll
+      for (int kq = 0; kq < NMB; ++kq) store4(rdn, eoff<D>(cur, 16 * kq + 4 * g), dnum[kq]);
+    }
   }
 
   float* rec = dsp + ((size_t)h * P.units + unit) * P.rec_floats;
   __syncthreads();  // every wave is done with its staging area
-  wave_ordered_sum<D>(acc3, sbuf, rec);
+  if constexpr (kDS) wave_ordered_sum<D>(acc3, sbuf, rec);
   reduce_sigma<D>(dzacc, red, rec + D * D);
   reduce_sigma<D>(dgacc, red, dgp + ((size_t)h * P.units + unit) * D);
+}
+
+// ---------------------------------------------------------------------------
+// dS of a unit from the query pass's dnum (d = 128): dS_p = sum_i Qh_i dnum_i^T
+// with Qh recomputed exactly as the query pass forms it, the tokens taken in
+// the same order (each wave its contiguous quarter, 16 at a time; the four
+// waves' partials added in wave order).  Writes S-part of the unit's record;
+// the query pass wrote its dz part.
+// ---------------------------------------------------------------------------
+template <typename T, int D>
+__global__ void __launch_bounds__(kThreads, 1)
+bwd_dsum_mfma_kernel(Plan P, const T* __restrict__ qin, const float* __restrict__ dnum,
+                     const float* __restrict__ conv_w, const int32_t* __restrict__ cu,
+                     float* __restrict__ dsp) {
+  using C = MF<D>;
+  constexpr int NMB = C::NMB;
+  __shared__ __attribute__((aligned(16))) float stg[4][2][C::kStage];  // [wave][Qh or dnum]
+  __shared__ f32x4_t tq[D];
+  static_assert(sizeof(stg) >= D * D * sizeof(float), "staging holds a d x d matrix");
+  const int tid = threadIdx.x, lane = tid & 63, n = lane & 15, g = lane >> 4;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int h = blockIdx.y, unit = blockIdx.x;
+  int s, chunk;
+  if (!unit_of(P, cu, P.chunk, P.chunks_per_seq, unit, &s, &chunk)) return;
+  int64_t len, base_row;
+  seq_geometry(P, cu, s, h, &len, &base_row);
+  const int t0 = chunk * P.chunk;
+  const int t1 = (int)min(len, (int64_t)t0 + P.chunk);
+  if (tid < D) {
+    float w4[4];
+    load_taps4(conv_w, P.heads, h, 0, D, P.W, tid, w4);
+    tq[tid] = (f32x4_t){w4[0], w4[1], w4[2], w4[3]};
+  }
+  __syncthreads();
+  const uint32_t rows = (uint32_t)len * D;
+  const __amdgpu_buffer_rsrc_t rq = make_rsrc(qin + base_row * D, rows * sizeof(T));
+  const __amdgpu_buffer_rsrc_t rdn = make_rsrc(dnum + base_row * D, rows * 4u);
+  f32x4_t acc[C::kBlocks];
+#pragma unroll
+  for (int k = 0; k < C::kBlocks; ++k) acc[k] = (f32x4_t){0.0f, 0.0f, 0.0f, 0.0f};
+  float* X = stg[wave][0];
+  float* Y = stg[wave][1];
+
+  const int q4 = P.chunk / 4, w0 = t0 + wave * q4, w1 = min(t1, w0 + q4);
+  RowStream<T, D> sq;
+  u32x4_t dnraw[NMB];
+  int tok = w0 + n;
+  auto issue_dn = [&](int tk) {
+#pragma unroll
+    for (int kq = 0; kq < NMB; ++kq) dnraw[kq] = Raw<float>::load(rdn, eoff<D>(tk, 16 * kq + 4 * g));
+  };
+  sq.start(rq, tok, g);
+  issue_dn(tok);
+  for (int b0 = w0; b0 < w1; b0 += 16) {
+    float qh[NMB][4], dn[NMB][4];
+    __asm__ volatile("" ::: "memory");  // taps are re-read from LDS, not held
+    sq.conv(tq, g, qh);
+#pragma unroll
+    for (int kq = 0; kq < NMB; ++kq) {
+      const f32x4_t d = Raw<float>::widen(dnraw[kq]);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        qh[kq][i] = phi_fast(qh[kq][i]);
+        dn[kq][i] = d[i];
+      }
+    }
+    tok += 16;
+    sq.issue(rq, tok, g);  // the next block's rows (out of range past the slice: 0, unused)
+    issue_dn(tok);
+    wave_lds_sync();  // the previous block's reads of X, Y are done
+    stage_sigma<D>(X, n, g, qh);
+    stage_sigma<D>(Y, n, g, dn);
+    wave_lds_sync();
+    token_product<D>(X, Y, lane, acc);
+  }
+  float* rec = dsp + ((size_t)h * P.units + unit) * P.rec_floats;
+  __syncthreads();  // every wave is done with its staging area
+  wave_ordered_sum<D>(acc, &stg[0][0][0], rec);
 }
 
 // ---------------------------------------------------------------------------
@@ -1201,7 +1336,7 @@ bwd_query_mfma_kernel(Plan P, const T* __restrict__ qin, const T* __restrict__ r
 // 16-token blocks independently.
 // ---------------------------------------------------------------------------
 template <typename T, int D>
-__global__ void __launch_bounds__(kThreads, 2)
+__global__ void __launch_bounds__(kThreads, D >= 128 ? 1 : 2)
 bwd_key_mfma_kernel(Plan P, const T* __restrict__ kin, const T* __restrict__ vin,
                     const T* __restrict__ ain, const float* __restrict__ conv_w,
                     const int32_t* __restrict__ cu, const float* __restrict__ dSg,
@@ -1211,7 +1346,9 @@ bwd_key_mfma_kernel(Plan P, const T* __restrict__ kin, const T* __restrict__ vin
   constexpr int NMB = C::NMB;
   __shared__ f32x4_t a4[NMB * NMB * 64];  // t = dS vt: A[c][e] = dS[c][e]
   __shared__ f32x4_t a5[NMB * NMB * 64];  // dvt = dS^T P: A[e][c] = dS[c][e]
-  __shared__ __attribute__((aligned(16))) float sbuf[D * D];
+  // dS staged for the layouts (d <= 64; at d = 128 they are built from memory)
+  constexpr bool kStaged = D <= 64;
+  __shared__ __attribute__((aligned(16))) float sbuf[kStaged ? D * D : 4];
   __shared__ f32x4_t tk[D], tv[D];
   __shared__ __attribute__((aligned(16))) float dzs[D];
   const int tid = threadIdx.x, lane = tid & 63, n = lane & 15, g = lane >> 4;
@@ -1225,7 +1362,7 @@ bwd_key_mfma_kernel(Plan P, const T* __restrict__ kin, const T* __restrict__ vin
   const int t1 = (int)min(len, (int64_t)t0 + P.chunk);
   const size_t sh = (size_t)s * P.heads + h;
   const float* dS = dSg + sh * (D * D + D);
-  stage_matrix<D>(dS, sbuf);
+  if constexpr (kStaged) stage_matrix<D>(dS, sbuf);
   if (tid < D) {
     float w4[4];
     load_taps4(conv_w, P.heads, h, 1, D, P.W, tid, w4);
@@ -1237,8 +1374,8 @@ bwd_key_mfma_kernel(Plan P, const T* __restrict__ kin, const T* __restrict__ vin
   const float M = mz[2 * sh], Z = mz[2 * sh + 1];
   const float invZ = Z > 0.0f ? 1.0f / Z : 0.0f;
   __syncthreads();
-  build_frags<D, false>(sbuf, a4);
-  build_frags<D, true>(sbuf, a5);
+  build_frags<D, false>(kStaged ? sbuf : dS, a4);
+  build_frags<D, true>(kStaged ? sbuf : dS, a5);
   __syncthreads();
 
   const uint32_t rows = (uint32_t)len * D;
@@ -1404,33 +1541,37 @@ gbla_status run_backward(const Plan& p, const BwdLayout& L, const void* q, const
   float* dcp = reinterpret_cast<float*>(base + L.off_dcp);
   const size_t act_elems = (size_t)p.tokens * p.heads * D;
   const dim3 grid(p.units, p.heads);
-  // Matrix-core kernels for head dims 32 and 64; 32-bit buffer offsets need
-  // every fp32 (sequence, head) slice below 2^31 bytes.
+  // Matrix-core kernels for every head dim; 32-bit buffer offsets need every
+  // fp32 (sequence, head) slice below 2^31 bytes.
   const bool small_slices = (int64_t)p.rows * D * 4 < (int64_t(1) << 31);
   constexpr int kElems = D * D + D;
   const dim3 cgrid((unsigned)((int64_t)p.nseq * p.heads), (kElems + kThreads - 1) / kThreads);
-  bool mfma = false;
-  if constexpr (D == 32 || D == 64) mfma = small_slices;
-  if constexpr (D == 32 || D == 64) {
-    if (mfma) {
-      hipLaunchKernelGGL((bwd_state_mfma_kernel<T, D>), grid, dim3(kThreads), 0, st, p,
-                         (const T*)k, (const T*)v, (const T*)a, conv_w, cu, dsp);
-      gbla_status e = launch_combine_f32(p, cu, dsp, S, z, mz, st);
-      if (e != GBLA_OK) return e;
-      if (gamma)
-        hipLaunchKernelGGL((bwd_query_mfma_kernel<T, D, true>), grid, dim3(kThreads), 0, st, p,
-                           (const T*)q, (const T*)r, dy, conv_w, gamma, cu, (const float*)S,
-                           (const float*)z, dxt, dr, dsp, dgp);
-      else
-        hipLaunchKernelGGL((bwd_query_mfma_kernel<T, D, false>), grid, dim3(kThreads), 0, st, p,
-                           (const T*)q, (const T*)r, dy, conv_w, gamma, cu, (const float*)S,
-                           (const float*)z, dxt, dr, dsp, dgp);
-      hipLaunchKernelGGL((bwd_dscombine_kernel<D>), cgrid, dim3(kThreads), 0, st, p, cu,
-                         (const float*)dsp, dS);
-      hipLaunchKernelGGL((bwd_key_mfma_kernel<T, D>), grid, dim3(kThreads), 0, st, p,
-                         (const T*)k, (const T*)v, (const T*)a, conv_w, cu, (const float*)dS,
-                         (const float*)mz, dxt + act_elems, dxt + 2 * act_elems, da);
-    }
+  bool mfma = small_slices;
+  if (mfma) {
+    // d = 128: the query pass writes dnum into the third dxt slot (the key
+    // pass fills it only afterwards) and bwd_dsum_mfma_kernel sums dS from it
+    constexpr bool kDS = D <= 64;
+    float* dnum = dxt + 2 * act_elems;
+    hipLaunchKernelGGL((bwd_state_mfma_kernel<T, D>), grid, dim3(kThreads), 0, st, p,
+                       (const T*)k, (const T*)v, (const T*)a, conv_w, cu, dsp);
+    gbla_status e = launch_combine_f32(p, cu, dsp, S, z, mz, st);
+    if (e != GBLA_OK) return e;
+    if (gamma)
+      hipLaunchKernelGGL((bwd_query_mfma_kernel<T, D, true, kDS>), grid, dim3(kThreads), 0, st, p,
+                         (const T*)q, (const T*)r, dy, conv_w, gamma, cu, (const float*)S,
+                         (const float*)z, dxt, dr, dsp, dgp, dnum);
+    else
+      hipLaunchKernelGGL((bwd_query_mfma_kernel<T, D, false, kDS>), grid, dim3(kThreads), 0, st, p,
+                         (const T*)q, (const T*)r, dy, conv_w, gamma, cu, (const float*)S,
+                         (const float*)z, dxt, dr, dsp, dgp, dnum);
+    if constexpr (!kDS)
+      hipLaunchKernelGGL((bwd_dsum_mfma_kernel<T, D>), grid, dim3(kThreads), 0, st, p,
+                         (const T*)q, (const float*)dnum, conv_w, cu, dsp);
+    hipLaunchKernelGGL((bwd_dscombine_kernel<D>), cgrid, dim3(kThreads), 0, st, p, cu,
+                       (const float*)dsp, dS);
+    hipLaunchKernelGGL((bwd_key_mfma_kernel<T, D>), grid, dim3(kThreads), 0, st, p,
+                       (const T*)k, (const T*)v, (const T*)a, conv_w, cu, (const float*)dS,
+                       (const float*)mz, dxt + act_elems, dxt + 2 * act_elems, da);
   }
   if (!mfma) {
     hipLaunchKernelGGL((bwd_state_kernel<T, D>), grid, dim3(kThreads), 0, st, p, (const T*)k,
