@@ -842,12 +842,16 @@ __device__ __forceinline__ void stage_sigma(float* arr, int n, int g, const floa
 // acc[mb * NMB + nb] += sum over the wave's 16 staged tokens of X[tok][c]
 // Y[tok][e] for c block mb, e block nb (K step kk is token 4 kk + g of lane
 // group g).
+// With zpart, also zpart[b] += X[tok][16 b + j] over the lane's tokens
+// (tokens g, g + 4, ... of lane (j, g)): the column sums of X.
 template <int D>
 __device__ __forceinline__ void token_product(const float* X, const float* Y, int lane,
-                                              f32x4_t* acc) {
+                                              f32x4_t* acc, float* zpart = nullptr) {
   using C = MF<D>;
   const int j = lane & 15, g = lane >> 4;
-#pragma unroll
+  // at d = 128 (64 products per K step) the K steps are not unrolled, so that
+  // their reads are not all hoisted into registers at once
+#pragma unroll(D >= 128 ? 1 : 4)
   for (int kk = 0; kk < 4; ++kk) {
     const int row = (4 * kk + g) * C::kRow;
     float xv[C::NMB], yv[C::NMB];
@@ -861,6 +865,10 @@ __device__ __forceinline__ void token_product(const float* X, const float* Y, in
 #pragma unroll
       for (int nb = 0; nb < C::NMB; ++nb)
         acc[mb * C::NMB + nb] = mfma4(xv[mb], yv[nb], acc[mb * C::NMB + nb]);
+    if (zpart) {
+#pragma unroll
+      for (int b = 0; b < C::NMB; ++b) zpart[b] += xv[b];
+    }
   }
 }
 
@@ -961,11 +969,11 @@ bwd_state_mfma_kernel(Plan P, const T* __restrict__ kin, const T* __restrict__ v
   f32x4_t acc[C::kBlocks];
 #pragma unroll
   for (int k = 0; k < C::kBlocks; ++k) acc[k] = (f32x4_t){0.0f, 0.0f, 0.0f, 0.0f};
-  float zacc[NMB][4];
+  // z: the column sums of the staged gated keys, per lane (channel 16 b + j,
+  // tokens g, g + 4, ...), summed over the lane groups and waves at the end
+  float zpart[NMB];
 #pragma unroll
-  for (int kq = 0; kq < NMB; ++kq)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) zacc[kq][i] = 0.0f;
+  for (int b = 0; b < NMB; ++b) zpart[b] = 0.0f;
   float lacc = 0.0f;
   float* X = stg[wave][0];
   float* Y = stg[wave][1];
@@ -992,21 +1000,24 @@ bwd_state_mfma_kernel(Plan P, const T* __restrict__ kin, const T* __restrict__ v
 #pragma unroll
     for (int kq = 0; kq < NMB; ++kq)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        kt[kq][i] = w * phi_fast(kt[kq][i]);
-        zacc[kq][i] += kt[kq][i];
-      }
+      for (int i = 0; i < 4; ++i) kt[kq][i] = w * phi_fast(kt[kq][i]);
     wave_lds_sync();  // the previous block's reads of X, Y are done
     stage_sigma<D>(X, n, g, kt);
     stage_sigma<D>(Y, n, g, vt);
     wave_lds_sync();
-    token_product<D>(X, Y, lane, acc);
+    token_product<D>(X, Y, lane, acc, zpart);
   }
 
   float* rec = partials + ((size_t)h * P.units + unit) * P.rec_floats;
   __syncthreads();  // every wave is done with its staging area
   wave_ordered_sum<D>(acc, &stg[0][0][0], rec);
-  reduce_sigma<D>(zacc, red, rec + D * D);
+#pragma unroll
+  for (int b = 0; b < NMB; ++b) {
+    const float zs = sum_groups(zpart[b]);
+    if (g == 0) red[wave][16 * b + n] = zs;
+  }
+  __syncthreads();
+  if (tid < D) rec[D * D + tid] = ((red[0][tid] + red[1][tid]) + red[2][tid]) + red[3][tid];
   const float lsum = sum_tokens(lacc);  // lanes of group 0 hold the weights
   if (lane == 0) red4[wave] = lsum;
   __syncthreads();
