@@ -123,8 +123,9 @@ def test_backward_parity_full_size(G, dev, name):
 
 
 # Ablation switches (the paper's ablation table): each alone and all three
-# (BLA, Eq. (1)), through both kernel families (d = 32 / 64 on the matrix
-# cores, d = 128 on the vector path), dense and ragged.
+# (BLA, Eq. (1)), through both matrix-core arrangements (d = 32 / 64 with dS
+# summed in the query pass, d = 128 with its separate dS pass), dense and
+# ragged.
 SWITCH_CASES = ["bf16_d64_n1000", "f32_d64_n1000", "ragged_d128_mixed", "bf16_d32_n3001_W2"]
 
 
