@@ -4,19 +4,23 @@
 // conv_x_kernel  streams X once: causal depthwise conv in fp32, Xt rounded
 //                to bf16 into the workspace (a bf16 layer stores it so).
 // proj_kernel    P = Xt Wp^T on v_mfma_f32_32x32x16_bf16 (fp32 accumulation):
-//                a workgroup of 8 waves (2 x 4, 128 x 64 each) computes a
-//                256-token x 256-feature tile, 64 model channels per K step,
-//                the next steps' rows loaded into registers while the
-//                current step's products run.  The epilogue rounds P to bf16
-//                and scatters every feature to the head-major layout the
-//                attention kernels read ([B, H, n, d] / [B, H, n]), through
-//                LDS so that each lane writes 16-byte pieces.
+//                a workgroup of 4 waves (2 x 2, 128 x 128 each, one per
+//                SIMD, accumulators in AGPRs) computes a 256-token x
+//                256-feature tile, 32 model channels per K step, the
+//                operand rows loaded straight into a four-step LDS ring
+//                three steps ahead.  The output is rounded to bf16 and
+//                scattered to the head-major layout the attention kernels
+//                read ([B, H, n, d] / [B, H, n]), written under the next
+//                tile's products where the shape allows.
 // The conv is a separate pass rather than part of the tile staging: redone
 // for every feature tile, its vector work would compete with the products
 // (measured: 0.36 against 0.54 PFLOP/s for the GEMM), while the pass itself
 // costs one read and one write of X.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+
+#include <type_traits>
+#include <utility>
 
 #include "gbla_device.h"
 #include "gbla_ext.h"
@@ -26,40 +30,62 @@ namespace gbla {
 namespace {
 
 constexpr int kBM = 256, kBN = 256, kBK = 32;
-constexpr int kProjWaves = 8, kProjThreads = 64 * kProjWaves;  // 2 x 4 waves
+constexpr int kProjWaves = 4, kProjThreads = 64 * kProjWaves;  // 2 x 2 waves
 constexpr int kProjGrid = 256;                                  // persistent workgroups
-constexpr int kWaveM = kBM / 2, kWaveN = kBN / 4;               // 128 x 64 per wave
+constexpr int kWaveM = kBM / 2, kWaveN = kBN / 2;               // 128 x 128 per wave
 constexpr int kRowBytes = kBK * 2;           // one tile row of bf16: four 16-byte chunks
 constexpr int kTileBytes = 256 * kRowBytes;  // 16 KB
-// LDS: two K steps of both tiles, or in the epilogue a 64 x 64 half of
-// every wave's tile in bf16, rows padded to 72 elements
-constexpr int kEpRow = 72;
-constexpr int kLdsBytes = 4 * kTileBytes > kProjWaves * 64 * kEpRow * 2 ? 4 * kTileBytes
-                                                                         : kProjWaves * 64 * kEpRow * 2;
+constexpr int kStages = 4;                   // K steps held in LDS at once
+constexpr int kStageBytes = 2 * kTileBytes;  // both tiles of one K step
+constexpr int kLdsBytes = kStages * kStageBytes;
+// per wave and K step: 16-byte loads into LDS, 1 KB (64 lanes) each
+constexpr int kDmaPerTile = kTileBytes / (kProjThreads * 16);
 
 // Byte offset of 16-byte chunk `c` of row `r` in a tile.  The chunks are
 // XOR-swizzled by r / 4: a 16-byte operand read serves 16 lanes (16
 // consecutive rows) per cycle from 64 banks (256 bytes), and four rows share
 // a 256-byte bank row, so the four rows of a bank row take its four chunks
-// and the swizzle gives the four groups of four rows different chunks.  (The
-// signed division, rather than a shift, keeps the compiler from holding a
-// precomputed address per operand across the loop, which made it spill.)
-__device__ __forceinline__ int tile_off(int r, int c) { return r * kRowBytes + ((c ^ ((r / 4) & 3)) << 4); }
+// and the swizzle gives the four groups of four rows different chunks.
+__device__ __forceinline__ int tile_off(int r, int c) { return r * kRowBytes + ((c ^ ((r >> 2) & 3)) << 4); }
+
+// A buffer resource over `bytes` bytes from `base`, as four scalar registers
+// for the assembly loads below (the same descriptor as make_rsrc).
+__device__ __forceinline__ u32x4_t rsrc_sgprs(const void* base, uint32_t bytes) {
+  const uint64_t ad = reinterpret_cast<uint64_t>(base);
+  return u32x4_t{(uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)ad),
+                 (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(ad >> 32)),
+                 (uint32_t)__builtin_amdgcn_readfirstlane((int)bytes), 0x00020000u};
+}
+
+// 16 bytes per lane from the buffer into LDS at base + 16 * lane (M0 = base;
+// one wait state after writing M0).  Assembly, so that the compiler neither
+// tracks these loads (the step loop waits for them explicitly, by count) nor
+// moves LDS accesses across them.
+__device__ __forceinline__ void dma16(const u32x4_t& r, unsigned char* base, uint32_t off) {
+  const uint32_t m = (uint32_t)__builtin_amdgcn_readfirstlane(
+      (int)(uint32_t)(uintptr_t)(__attribute__((address_space(3))) void*)base);
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds"
+               :
+               : "v"(off), "s"(r), "s"(m)
+               : "memory", "m0");
+}
+
+// s_waitcnt vmcnt(N), the other counters left alone (gfx9 encoding).
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x0F70);
+}
+
+// Workgroup barrier with no fence: a fence would make each wave wait for all
+// of its loads in flight, the later K steps' too.  Each wave has waited for
+// its own loads of the step it reads next, and every LDS read of a stage is
+// consumed (so complete) before the barrier after which that stage is
+// refilled.  The clobber keeps the compiler from moving LDS accesses across.
+__device__ __forceinline__ void step_sync() { asm volatile("s_barrier" ::: "memory"); }
 
 __device__ __forceinline__ u32x4_t bload(__amdgpu_buffer_rsrc_t r, uint32_t off) {
   return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
-}
-
-// fp32 -> bf16 bits, round to nearest even, in integer arithmetic.  In the
-// projection epilogue, the hardware pack conversion or any per-element NaN
-// select made the register allocator spill the main loop's accumulators.
-// No select is needed there: the only NaNs an accumulator can hold are the
-// default NaN or NaNs carried from bf16 inputs, whose low 16 bits are zero,
-// and for those the rounding sum cannot carry into bit 16, so they keep
-// their upper half (a NaN).
-__device__ __forceinline__ uint16_t bf16_bits_rne(float f) {
-  const uint32_t u = __float_as_uint(f);
-  return (uint16_t)((u + 0x7fffu + ((u >> 16) & 1u)) >> 16);
 }
 
 // First token of the sequence that holds token m (global token index).
@@ -146,29 +172,60 @@ conv_x_kernel(LayerPlan P, const uint16_t* __restrict__ x, const float* __restri
 // ---------------------------------------------------------------------------
 // proj_kernel: P = Xt Wp^T on bf16 MFMA, scattered to the attention layout.
 // (features / 256) x (tokens / 256) tiles, numbered L, owned by persistent
-// workgroups (tiles blockIdx.x, blockIdx.x + gridDim.x, ...); 8 waves
-// (2 x 4) of 128 x 64, two per SIMD, so one workgroup per CU (244 VGPRs a
-// wave).  A wave tile of 128 x 64 reads 0.75 KB of LDS operands per 32x32x16
-// product, against 1 KB for 64 x 64, and the larger workgroup tile halves
-// the L2 reads per product.  The dispatcher places workgroup b on XCD b % 8;
-// with a grid that is a multiple of 8, tile L therefore runs on XCD L % 8.
-// When the token tiles come in multiples of 64, each XCD takes every eighth
-// token tile in groups of eight, walking all feature tiles of a group before
-// the next, so that the workgroups an XCD holds at once share a few token
-// and feature tiles in its L2, where the plain order made every XCD stream
-// all of Wp.
+// workgroups (tiles blockIdx.x, blockIdx.x + gridDim.x, ...).  Four waves
+// (2 x 2) of 128 x 128, one per SIMD: a wave's accumulators fill its 256
+// AGPRs, and a 128 x 128 wave tile reads 0.5 KB of LDS operands per
+// 32x32x16 product.
+//
+// The K steps of all the workgroup's tiles form one stream, numbered g:
+// step g sits in LDS stage g % 4, loaded by buffer loads that write LDS
+// directly (no staging registers, no LDS stores) three steps ahead.  At the
+// top of step g every wave waits for its own loads of step g + 1 and the
+// workgroup meets at a barrier; the loads of step g + 3 then refill the
+// stage of step g - 1, issued between the step's first products.  A wave
+// reads its slice-1 operands of step g and its slice-0 operands of step
+// g + 1 while the products of the step run, so the products after a
+// barrier never wait for LDS.
+//
+// Output: the products are formed as P^T (Wp rows as the first operand),
+// so lane l of a 32 x 32 block holds token l % 32 and, in elements
+// 4 g .. 4 g + 3, the four consecutive features 8 g + 4 (l / 32) .. + 3.
+// Stores must cover whole lines: 16 bytes per lane at different tokens'
+// rows cost an L2 request each, which made the output as slow as the
+// products.  So with DEFER (d_model a multiple of 1024, i.e. at least 32 K
+// steps per tile; a tile's features in one of q, k, v, r; its tokens' rows
+// linear) each wave stages its block through LDS at the tile's end and
+// reads it back as 16-byte pieces, eight lanes to a 128-byte row, which go
+// out one per K step of the next tile, under its products.  Every step then
+// issues exactly one store (to an out-of-range offset when none is
+// pending), so the load waits keep exact counts.  Without DEFER, and for
+// the tile holding the gate logits (destinations H rows apart, written one
+// by one), the tile is written from the accumulators at once (eight bytes
+// per lane) and, with DEFER, drained.
+//
+// The dispatcher places workgroup b on XCD b % 8; with a grid that is a
+// multiple of 8, tile L therefore runs on XCD L % 8.  When the token tiles
+// come in multiples of 64, each XCD takes every eighth token tile in groups
+// of eight, walking all feature tiles of a group before the next, so that
+// the workgroups an XCD holds at once share a few token and feature tiles
+// in its L2, where the plain order made every XCD stream all of Wp.
 // ---------------------------------------------------------------------------
+template <int... U, class F>
+__device__ __forceinline__ void unrolled(std::integer_sequence<int, U...>, F&& f) {
+  (f(std::integral_constant<int, U>{}), ...);
+}
+
+template <bool DEFER>
 __global__ void __launch_bounds__(kProjThreads, 1)
 proj_kernel(LayerPlan P, const uint16_t* __restrict__ xt, const uint16_t* __restrict__ wp,
             uint16_t* __restrict__ q, uint16_t* __restrict__ k, uint16_t* __restrict__ v,
             uint16_t* __restrict__ r, uint16_t* __restrict__ a) {
-  // two K steps of both tiles ([buf][Xt or W]); the epilogue reuses it
-  __shared__ __attribute__((aligned(16))) unsigned char lds_raw[kLdsBytes];
-  auto tile = [&](int buf, int which) { return lds_raw + (2 * buf + which) * kTileBytes; };
-  constexpr int TM = kWaveM / 32, TN = kWaveN / 32;   // 32 x 32 products per wave and K slice
-  constexpr int kLoads = kBM * (kBK / 8) / kProjThreads;  // 16-byte pieces per thread and tile
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 2, wn = wave & 3;
+  __shared__ __attribute__((aligned(1024))) unsigned char lds[kLdsBytes];
+  constexpr int TM = kWaveM / 32, TN = kWaveN / 32;  // 32 x 32 products per wave and K slice
+  constexpr int kStoresPerStep = 1;  // deferred 16-byte stores per lane and K step
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 1, wn = wave & 1;
   const int tiles_n = (P.features + kBN - 1) / kBN, tiles_m = (P.tokens + kBM - 1) / kBM;
   const int tiles = tiles_n * tiles_m;
   // token and feature tile bases of tile L
@@ -187,172 +244,285 @@ proj_kernel(LayerPlan P, const uint16_t* __restrict__ xt, const uint16_t* __rest
     n0_ = tn * kBN;
   };
   const int K = P.d_model, M = P.tokens, N = P.features;
-  const __amdgpu_buffer_rsrc_t rx = make_rsrc(xt, (uint32_t)((int64_t)M * K * 2));
-  const __amdgpu_buffer_rsrc_t rw = make_rsrc(wp, (uint32_t)((int64_t)N * K * 2));
-
   const int nk = K / kBK;
-  // Register staging, two K steps ahead: set s holds the rows of every
-  // other step, so a step's rows have two steps of products to arrive.
-  u32x4_t xraw[2][kLoads], wraw[2][kLoads];
-  // Steps past the last load out of range (zeros, no traffic): the loads are
-  // never behind a branch, so the compiler's waits stay exact (a branch made
-  // it drain every load before each commit).
-  auto issue = [&](int set, int kt, int m0, int n0, bool tile_live) {
-    const int k0 = kt * kBK;
-    const bool live = tile_live && kt < nk;
-    // 32-bit offsets: tokens * d_model * 2 < 2^31 (the plan checks it), so
-    // even a row up to 255 past the last token stays below 2^32
+  const int Hd = P.heads * P.d;
+  const int64_t hstride = P.ragged ? (int64_t)M : (int64_t)P.rows;  // rows between heads
+  const int half = lane >> 5, l32 = lane & 31;
+
+  // ---- the load stream ----
+  // Load j of a wave covers tile rows 16 (kDmaPerTile wave + j) .. + 15: lane
+  // l writes row (l / 4), stored chunk l % 4, which holds source chunk
+  // (l % 4) ^ (row / 4 % 4) (the swizzle of tile_off).  The offsets within the
+  // tile are the same for Xt and Wp; the tile's first row and the K step go
+  // into the descriptor, whose extent ends at the last token (feature), so
+  // rows past it read zeros.
+  uint32_t loff[kDmaPerTile];
 #pragma unroll
-    for (int j = 0; j < kLoads; ++j) {
-      const int c = tid + kProjThreads * j, row = c >> 2, ch = c & 3;
-      xraw[set][j] = bload(rx, live ? ((uint32_t)(m0 + row) * (uint32_t)K + (uint32_t)(k0 + 8 * ch)) * 2u : kOutOfRange);
-    }
-#pragma unroll
-    for (int j = 0; j < kLoads; ++j) {
-      const int c = tid + kProjThreads * j, row = c >> 2, ch = c & 3;
-      wraw[set][j] = bload(rw, live ? ((uint32_t)(n0 + row) * (uint32_t)K + (uint32_t)(k0 + 8 * ch)) * 2u : kOutOfRange);
-    }
+  for (int j = 0; j < kDmaPerTile; ++j) {
+    const int row = 16 * (kDmaPerTile * wave + j) + (lane >> 2);
+    const int ch = (lane & 3) ^ ((lane >> 4) & 3);
+    loff[j] = (uint32_t)(row * K + 8 * ch) * 2u;
+  }
+  int dL = blockIdx.x, ds = 0, dm0 = 0, dn0 = 0;  // the next step to load
+  if (dL < tiles) tile_of(dL, dm0, dn0);
+  u32x4_t lrx, lrw;
+  unsigned char* lst;
+  auto load_prep = [&](int stage) {
+    const bool live = dL < tiles;
+    const int k0 = ds * kBK;
+    const uint32_t xb = live && dm0 < M ? (uint32_t)(((int64_t)(M - dm0) * K - k0) * 2) : 0u;
+    const uint32_t wb = live ? (uint32_t)(((int64_t)(N - dn0) * K - k0) * 2) : 0u;
+    lrx = rsrc_sgprs(xt + ((int64_t)dm0 * K + k0), xb);
+    lrw = rsrc_sgprs(wp + ((int64_t)dn0 * K + k0), wb);
+    lst = lds + stage * kStageBytes + wave * (kDmaPerTile * 1024);
   };
-  auto commit = [&](int set, int buf) {
-#pragma unroll
-    for (int j = 0; j < kLoads; ++j) {
-      const int c = tid + kProjThreads * j, row = c >> 2, ch = c & 3;
-      *reinterpret_cast<u32x4_t*>(tile(buf, 0) + tile_off(row, ch)) = xraw[set][j];
-    }
-#pragma unroll
-    for (int j = 0; j < kLoads; ++j) {
-      const int c = tid + kProjThreads * j, row = c >> 2, ch = c & 3;
-      *reinterpret_cast<u32x4_t*>(tile(buf, 1) + tile_off(row, ch)) = wraw[set][j];
+  auto load_part = [&](int j) {
+    dma16(lrx, lst + 1024 * j, loff[j]);
+    dma16(lrw, lst + kTileBytes + 1024 * j, loff[j]);
+  };
+  auto load_advance = [&]() {
+    if (++ds == nk) {
+      ds = 0;
+      dL += gridDim.x;
+      if (dL < tiles) tile_of(dL, dm0, dn0);
     }
   };
 
+  // ---- operand reads and products ----
+  // The operand of lane l in K slice ks: row l % 32 of a 32-row block, chunk
+  // 2 ks + l / 32.  Blocks start at multiples of 32 rows, so the swizzle
+  // depends on the lane only: one offset per slice, the block and stage
+  // added.
+  int roff[2];
+#pragma unroll
+  for (int ks = 0; ks < 2; ++ks) roff[ks] = tile_off(l32, 2 * ks + half);
+  u32x4_t fa[2][TM], fb[2][TN];  // [slice][block]
+  auto read_slice = [&](int stage, int ks) {
+    const unsigned char* A = lds + stage * kStageBytes + kWaveM * wm * kRowBytes + roff[ks];
+    const unsigned char* B = lds + stage * kStageBytes + kTileBytes + kWaveN * wn * kRowBytes + roff[ks];
+#pragma unroll
+    for (int i = 0; i < TM; ++i) fa[ks][i] = *reinterpret_cast<const u32x4_t*>(A + 32 * i * kRowBytes);
+#pragma unroll
+    for (int j = 0; j < TN; ++j) fb[ks][j] = *reinterpret_cast<const u32x4_t*>(B + 32 * j * kRowBytes);
+  };
   f32x16_t acc[TM][TN];
-  const int half = lane >> 5, l32 = lane & 31;
-  auto products = [&](int buf) {
-    const unsigned char* A = tile(buf, 0);
-    const unsigned char* B = tile(buf, 1);
+  auto mfma = [&](int ks, int i, int j) {
+    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, fb[ks][j]),
+                                                        __builtin_bit_cast(bf16x8_t, fa[ks][i]),
+                                                        acc[i][j], 0, 0, 0);
+  };
+
+  // ---- output ----
+  // Token row of (head 0, this lane's token m): [B, H, L, .] or [H, T, .].
+  auto token_row = [&](int m) -> int64_t {
+    if (P.ragged) return m;
+    const int b = m / P.rows;
+    return (int64_t)b * P.heads * P.rows + (m - b * P.rows);
+  };
+  // The whole tile at once (every tile without DEFER; gate-logit tiles).
+  auto write_now = [&](int m0, int n0) {
+    int64_t tokrow[TM];
+    bool tok_ok[TM];
 #pragma unroll
-    for (int ks = 0; ks < kBK / 16; ++ks) {
-      const int c = 2 * ks + half;
-      u32x4_t bf[TN];
+    for (int i = 0; i < TM; ++i) {
+      const int m = m0 + kWaveM * wm + 32 * i + l32;
+      tok_ok[i] = m < M;
+      tokrow[i] = token_row(m);
+    }
 #pragma unroll
-      for (int j = 0; j < TN; ++j)
-        bf[j] = *reinterpret_cast<const u32x4_t*>(B + tile_off(kWaveN * wn + 32 * j + l32, c));
+    for (int j = 0; j < TN; ++j) {
 #pragma unroll
-      for (int i = 0; i < TM; ++i) {
-        const u32x4_t af = *reinterpret_cast<const u32x4_t*>(A + tile_off(kWaveM * wm + 32 * i + l32, c));
+      for (int gq = 0; gq < 4; ++gq) {
+        const int nf = n0 + kWaveN * wn + 32 * j + 8 * gq;  // first feature of the group (uniform)
+        if (nf >= N) continue;
+        const bool in_proj = nf + 8 <= 4 * Hd;  // else gate logits (4 H d is a multiple of 8)
+        const int blk = in_proj ? nf / Hd : 0, h = in_proj ? (nf % Hd) / P.d : 0;
+        const int e = in_proj ? nf % P.d : 0;
+        uint16_t* const dst = blk == 0 ? q : blk == 1 ? k : blk == 2 ? v : r;
+        // the group's part of the address, the same for every lane
+        unsigned char* const gbase = reinterpret_cast<unsigned char*>(dst) + ((int64_t)h * hstride * P.d + e) * 2;
 #pragma unroll
-        for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, af),
-                                                              __builtin_bit_cast(bf16x8_t, bf[j]),
-                                                              acc[i][j], 0, 0, 0);
+        for (int i = 0; i < TM; ++i) {
+          if (!tok_ok[i]) continue;
+          const u32x2_t o{pack_bf16x2(acc[i][j][4 * gq], acc[i][j][4 * gq + 1]),
+                          pack_bf16x2(acc[i][j][4 * gq + 2], acc[i][j][4 * gq + 3])};
+          if (in_proj) {
+            *reinterpret_cast<u32x2_t*>(gbase + (tokrow[i] * P.d + 4 * half) * 2) = o;
+          } else {
+            for (int f = 0; f < 4; ++f) {
+              const int n = nf + 4 * half + f;
+              if (n < N) a[tokrow[i] + (n - 4 * Hd) * hstride] = (uint16_t)(o[f >> 1] >> (16 * (f & 1)));
+            }
+          }
+        }
       }
     }
   };
-  // A workgroup owns tiles blockIdx.x, blockIdx.x + gridDim.x, ...; the
-  // first two K steps of its next tile are loaded while the current tile's
-  // epilogue writes (out of range, no traffic, after its last tile).
-  int m0, n0;
-  tile_of(blockIdx.x, m0, n0);
-  issue(0, 0, m0, n0, true);
-  issue(1, 1, m0, n0, true);
-  for (int64_t L = blockIdx.x; L < tiles; L += gridDim.x) {
+  // Deferred output.  At a tile's end each wave stages its 128 x 128 bf16
+  // block, 32 tokens at a time, through the LDS stage of the tile's last
+  // step (rows of 256 bytes, 16-byte chunks XOR-swizzled by the row), and
+  // reads it back as 32 pieces of 16 bytes per lane: piece (i, pass) holds
+  // token 32 i + 4 pass + l / 16 and features 8 (l % 16) .. + 7, so eight
+  // lanes write one token's 128-byte row of a head (d = 64), whole lines.
+  // The features lie in one of q, k, v, r (H d is a multiple of 256) and the
+  // tile's tokens in one sequence or in the packed rows (token rows linear
+  // in the token); the targets' extents, tokens * H * d * 2 bytes, are
+  // below 2^31 (the launcher checks all three).
+  const uint32_t act_bytes = (uint32_t)((int64_t)M * Hd * 2);
+  u32x4_t ob[TM][8];
+  uint32_t obase = 0;   // byte offset of (this lane's first token, its features)
+  int mfirst = 0;       // this lane's first token
+  uint32_t tokstep = 0; // bytes between consecutive tokens' rows
+  __amdgpu_buffer_rsrc_t rcur = make_rsrc(q, 0u);
+  bool ob_live = false;
+  if constexpr (DEFER) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int ps = 0; ps < 8; ++ps) ob[i][ps] = u32x4_t{0u, 0u, 0u, 0u};
+  }
+  auto defer_tile = [&](int m0, int n0, unsigned char* stage) {
+    unsigned char* const wst = stage + wave * 8192;  // this wave's 32 x 256-byte rows
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+      // lane (token l32, half) writes features 32 j + 8 gq + 4 half .. + 3
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int gq = 0; gq < 4; ++gq) {
+          const int ch = (4 * j + gq) ^ (l32 & 15);
+          *reinterpret_cast<u32x2_t*>(wst + l32 * 256 + ch * 16 + 8 * half) =
+              u32x2_t{pack_bf16x2(acc[i][j][4 * gq], acc[i][j][4 * gq + 1]),
+                      pack_bf16x2(acc[i][j][4 * gq + 2], acc[i][j][4 * gq + 3])};
+        }
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+      for (int ps = 0; ps < 8; ++ps) {
+        const int row = 4 * ps + (lane >> 4);
+        ob[i][ps] = *reinterpret_cast<const u32x4_t*>(wst + row * 256 + (((lane & 15) ^ (row & 15)) * 16));
+      }
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    }
+    const int nf = n0 + kWaveN * wn, blk = nf / Hd;
+    const int c = nf % Hd + 8 * (lane & 15), h = c / P.d, e = c % P.d;
+    uint16_t* const dst = blk == 0 ? q : blk == 1 ? k : blk == 2 ? v : r;
+    rcur = make_rsrc(dst, act_bytes);
+    mfirst = m0 + kWaveM * wm + (lane >> 4);
+    obase = (uint32_t)(((token_row(mfirst) + (int64_t)h * hstride) * P.d + e) * 2);
+    tokstep = (uint32_t)(P.d * 2);
+  };
+  // Store PS of token block SB (its pieces rotate into ob[0], one block per
+  // eight steps); nothing pending past the fourth block.
+  auto store_slot = [&](auto ps_c, int sb) {
+    constexpr int ps = decltype(ps_c)::value;
+    const int dm = 32 * sb + 4 * ps;
+    const bool live = ob_live && sb < TM && mfirst + dm < M;
+    __builtin_amdgcn_raw_buffer_store_b128(ob[0][ps], rcur, live ? obase + dm * tokstep : kOutOfRange, 0, 0);
+  };
+
+  // ---- one K step ----
+  // With DEFER, steps come in blocks of eight from a step that is a multiple
+  // of 8, so step gg's stage is u % 4.
+  auto step = [&](int gg, auto u_c, int sb) {
+    constexpr int u = decltype(u_c)::value;
+    const int st = DEFER ? (u & (kStages - 1)) : (gg & (kStages - 1));
+    wait_vm<2 * kDmaPerTile + (DEFER ? 2 * kStoresPerStep : 0)>();  // own loads of step gg + 1 in
+    step_sync();  // everyone's; the stage of step gg - 1 is free
+    load_prep((st + 3) & (kStages - 1));
+    read_slice(st, 1);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {  // slice-0 products, a pair of loads after each row
+#pragma unroll
+      for (int j = 0; j < TN; ++j) mfma(0, i, j);
+      __builtin_amdgcn_sched_barrier(0);
+      load_part(i);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    load_advance();
+    read_slice((st + 1) & (kStages - 1), 0);  // the next step's (next tile's) first slice
+    // slice-1 products, the deferred store after the first half
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+#pragma unroll
+      for (int i = 2 * hh; i < 2 * hh + 2; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) mfma(1, i, j);
+      if constexpr (DEFER) {
+        if (hh == 0) {
+          __builtin_amdgcn_sched_barrier(0);
+          store_slot(u_c, sb);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
+    }
+  };
+
+  // ---- prologue: steps 0..2 in flight (each followed by two placeholder
+  // stores with DEFER), slice 0 of step 0 read ----
+#pragma unroll
+  for (int pstep = 0; pstep < kStages - 1; ++pstep) {
+    load_prep(pstep);
+#pragma unroll
+    for (int j = 0; j < kDmaPerTile; ++j) load_part(j);
+    load_advance();
+    if constexpr (DEFER) store_slot(std::integral_constant<int, 0>{}, TM);  // placeholder
+  }
+  wait_vm<2 * (2 * kDmaPerTile + (DEFER ? 2 * kStoresPerStep : 0))>();
+  step_sync();
+  read_slice(0, 0);
+
+  int g = 0;  // the step being multiplied
+  for (int L = blockIdx.x; L < tiles; L += gridDim.x) {
+    int m0, n0;
+    tile_of(L, m0, n0);
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
       for (int j = 0; j < TN; ++j)
 #pragma unroll
         for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
-    // Step kt's rows sit in set kt % 2 and LDS buffer kt % 2; the loop runs two
-    // steps per turn so that every staging index is a constant.
-    commit(0, 0);
-    __syncthreads();
-    for (int kt = 0; kt < nk; kt += 2) {
-      issue(0, kt + 2, m0, n0, true);  // set 0 is free: step kt is in LDS
-      products(0);
-      commit(1, 1);      // zeros past the last step, never read
-      __syncthreads();
-      if (kt + 1 >= nk) break;
-      issue(1, kt + 3, m0, n0, true);
-      products(1);
-      commit(0, 0);
-      __syncthreads();
-    }
-    int m1 = 0, n1 = 0;
-    const bool has_next = L + gridDim.x < tiles;
-    tile_of((int)(has_next ? L + gridDim.x : L), m1, n1);
-    issue(0, 0, m1, n1, has_next);
-    issue(1, 1, m1, n1, has_next);
-
-    // Epilogue, per 64 x 64 half of the wave's tile: through LDS as bf16 rows
-    // (stride 72 elements), then each lane writes 16-byte pieces: eight
-    // consecutive features of one token, which are eight consecutive channels
-    // of one head (d is a multiple of 8).  Gate-logit features, whose
-    // destinations are H rows apart, are written one by one.
-    uint16_t* ep = reinterpret_cast<uint16_t*>(lds_raw) + wave * 64 * kEpRow;
-    const int Hd = P.heads * P.d;
-    const int piece = lane & 7;                     // eight features 8 piece .. 8 piece + 7
-    const int nb = n0 + kWaveN * wn + 8 * piece;    // first feature of the piece
-    const bool in_proj = nb + 8 <= 4 * Hd;          // else gate logits (or past N)
-    const int blk = in_proj ? nb / Hd : 0, h = in_proj ? (nb % Hd) / P.d : 0, e = in_proj ? nb % P.d : 0;
-    uint16_t* const dst = blk == 0 ? q : blk == 1 ? k : blk == 2 ? v : r;
-    // Destination rows are linear in the token within a tile when its tokens
-    // are packed rows or lie in one dense sequence: then one row index per lane
-    // (for the tile's first token) and an offset per pass, with no division.
-    const bool linear = P.ragged || P.rows % kBM == 0;
-    int64_t b0 = 0, pos0 = m0;
-    if (!P.ragged) {
-      b0 = m0 / P.rows;
-      pos0 = m0 - b0 * P.rows;
-    }
-    auto out_row = [&](int head, int m) -> int64_t {  // row of (head, token m) in [.., n, d] / [H, T, d]
-      if (P.ragged) return (int64_t)head * M + m;
-      if (linear) return (b0 * P.heads + head) * P.rows + pos0 + (m - m0);
-      const int64_t b = m / P.rows;
-      return (b * P.heads + head) * P.rows + (m - b * P.rows);
-    };
+    if constexpr (DEFER) {
+      for (int s = 0, sb = 0; s < nk; s += 8, ++sb) {
+        unrolled(std::make_integer_sequence<int, 8>{}, [&](auto u_c) { step(g + decltype(u_c)::value, u_c, sb); });
+        g += 8;
 #pragma unroll
-    for (int si = 0; si < TM / 2; ++si) {
+        for (int i = 0; i + 1 < TM; ++i)  // the next token block's pieces
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j) {
-#pragma unroll
-          for (int rr = 0; rr < 16; ++rr) {
-            const int row = 32 * i + 8 * (rr >> 2) + 4 * half + (rr & 3);
-            ep[row * kEpRow + 32 * j + l32] = bf16_bits_rne(acc[2 * si + i][j][rr]);
-          }
-        }
-      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-      __builtin_amdgcn_wave_barrier();
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-#pragma unroll
-      for (int pass = 0; pass < 8; ++pass) {
-        const int row = 8 * pass + (lane >> 3);
-        const int m = m0 + kWaveM * wm + 64 * si + row;
-        if (m >= M || nb >= N) continue;
-        const uint16_t* src = ep + row * kEpRow + 8 * piece;
-        if (in_proj) {
-          *reinterpret_cast<u32x4_t*>(dst + out_row(h, m) * P.d + e) = *reinterpret_cast<const u32x4_t*>(src);
-        } else {
-#pragma unroll
-          for (int f = 0; f < 8; ++f) {
-            const int n = nb + f;
-            if (n >= N) break;
-            // gate logits (every earlier feature is in a 16-byte piece)
-            a[out_row(n - 4 * Hd, m)] = src[f];
-          }
-        }
+          for (int ps = 0; ps < 8; ++ps) ob[i][ps] = ob[i + 1][ps];
       }
-      // the next half reuses this wave's staging rows
-      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-      __builtin_amdgcn_wave_barrier();
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      if (n0 >= 4 * Hd) {  // gate logits (the last feature tile)
+        write_now(m0, n0);
+        wait_vm<0>();  // the variable number of stores drained: the counts stay exact
+        ob_live = false;
+      } else {
+        step_sync();  // every wave done reading the stage of the tile's last step
+        defer_tile(m0, n0, lds + ((g - 1) & (kStages - 1)) * kStageBytes);
+        ob_live = true;
+      }
+    } else {
+      for (int s = 0; s < nk; ++s, ++g) step(g, std::integral_constant<int, 0>{}, 0);
+      write_now(m0, n0);
     }
-    m0 = m1;
-    n0 = n1;
-    __syncthreads();  // every wave is done with the staging area before the next commit
   }
+  if constexpr (DEFER) {  // the last tile's stores
+    if (ob_live) {
+      for (int sb = 0; sb < TM; ++sb) {
+        unrolled(std::make_integer_sequence<int, 8>{}, [&](auto ps_c) { store_slot(ps_c, sb); });
+#pragma unroll
+        for (int i = 0; i + 1 < TM; ++i)
+#pragma unroll
+          for (int ps = 0; ps < 8; ++ps) ob[i][ps] = ob[i + 1][ps];
+      }
+    }
+  }
+  // drain: every load into LDS (the steps past the last tile read zeros)
+  // has landed before the workgroup ends
+  wait_vm<0>();
 }
 
 }  // namespace
@@ -368,9 +538,14 @@ gbla_status launch_project(const LayerPlan& p, const void* x, const float* conv_
   // one workgroup per CU (256 on MI355X), each owning every 256th tile; a
   // multiple of 8 keeps tile L on XCD L % 8
   const dim3 grid((unsigned)(tiles < kProjGrid ? tiles : kProjGrid));
-  hipLaunchKernelGGL(proj_kernel, grid, dim3(kProjThreads), 0, st, p, (const uint16_t*)xt,
-                     (const uint16_t*)w_proj, (uint16_t*)q, (uint16_t*)k, (uint16_t*)v,
-                     (uint16_t*)r, (uint16_t*)a);
+  // deferred stores: at least 32 K steps per tile, a tile's features in one
+  // target, its tokens' rows linear, and 32-bit offsets into q, k, v, r
+  const bool defer = p.d_model % 1024 == 0 && (p.heads * p.d) % 256 == 0 &&
+                     (p.ragged || p.rows % kBM == 0) &&
+                     (int64_t)p.tokens * p.heads * p.d * 2 < (int64_t(1) << 31);
+  hipLaunchKernelGGL(defer ? proj_kernel<true> : proj_kernel<false>, grid, dim3(kProjThreads), 0, st, p,
+                     (const uint16_t*)xt, (const uint16_t*)w_proj, (uint16_t*)q, (uint16_t*)k,
+                     (uint16_t*)v, (uint16_t*)r, (uint16_t*)a);
   return hipGetLastError() == hipSuccess ? GBLA_OK : GBLA_ERR_HIP;
 }
 
