@@ -37,7 +37,10 @@ constexpr int kRowBytes = kBK * 2;           // one tile row of bf16: four 16-by
 constexpr int kTileBytes = 256 * kRowBytes;  // 16 KB
 constexpr int kStages = 4;                   // K steps held in LDS at once
 constexpr int kStageBytes = 2 * kTileBytes;  // both tiles of one K step
-constexpr int kLdsBytes = kStages * kStageBytes;
+// the ring, then a spare 32 KB: one 32-token block of every wave's staged
+// output (the deferred stores' first eight)
+constexpr int kSpareBytes = 32768;
+constexpr int kLdsBytes = kStages * kStageBytes + kSpareBytes;
 // per wave and K step: 16-byte loads into LDS, 1 KB (64 lanes) each
 constexpr int kDmaPerTile = kTileBytes / (kProjThreads * 16);
 
@@ -61,13 +64,21 @@ __device__ __forceinline__ u32x4_t rsrc_sgprs(const void* base, uint32_t bytes) 
 // one wait state after writing M0).  Assembly, so that the compiler neither
 // tracks these loads (the step loop waits for them explicitly, by count) nor
 // moves LDS accesses across them.
-__device__ __forceinline__ void dma16(const u32x4_t& r, unsigned char* base, uint32_t off) {
-  const uint32_t m = (uint32_t)__builtin_amdgcn_readfirstlane(
-      (int)(uint32_t)(uintptr_t)(__attribute__((address_space(3))) void*)base);
+// M is the LDS byte address (wave-uniform).
+__device__ __forceinline__ void dma16(const u32x4_t& r, uint32_t m, uint32_t off) {
   asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds"
                :
                : "v"(off), "s"(r), "s"(m)
                : "memory", "m0");
+}
+
+// The lane index, computed where it is used: a volatile statement cannot be
+// hoisted, so addresses formed from it are not held (and spilled) across
+// the tile loop, where each reload's wait would drain the loads in flight.
+__device__ __forceinline__ int lane_now() {
+  int l;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(l));
+  return l;
 }
 
 // s_waitcnt vmcnt(N), the other counters left alone (gfx9 encoding).
@@ -219,14 +230,14 @@ template <bool DEFER>
 __global__ void __launch_bounds__(kProjThreads, 1)
 proj_kernel(LayerPlan P, const uint16_t* __restrict__ xt, const uint16_t* __restrict__ wp,
             uint16_t* __restrict__ q, uint16_t* __restrict__ k, uint16_t* __restrict__ v,
-            uint16_t* __restrict__ r, uint16_t* __restrict__ a) {
+            uint16_t* __restrict__ r) {
   __shared__ __attribute__((aligned(1024))) unsigned char lds[kLdsBytes];
   constexpr int TM = kWaveM / 32, TN = kWaveN / 32;  // 32 x 32 products per wave and K slice
   constexpr int kStoresPerStep = 1;  // deferred 16-byte stores per lane and K step
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;
-  const int tiles_n = (P.features + kBN - 1) / kBN, tiles_m = (P.tokens + kBM - 1) / kBM;
+  const int tiles_n = (4 * P.heads * P.d + kBN - 1) / kBN, tiles_m = (P.tokens + kBM - 1) / kBM;
   const int tiles = tiles_n * tiles_m;
   // token and feature tile bases of tile L
   auto tile_of = [&](int L, int& m0_, int& n0_) {
@@ -243,9 +254,9 @@ proj_kernel(LayerPlan P, const uint16_t* __restrict__ xt, const uint16_t* __rest
     m0_ = tm * kBM;
     n0_ = tn * kBN;
   };
-  const int K = P.d_model, M = P.tokens, N = P.features;
-  const int nk = K / kBK;
   const int Hd = P.heads * P.d;
+  const int K = P.d_model, M = P.tokens, N = 4 * Hd;  // Q, K, V, R features (the gates: gate_kernel)
+  const int nk = K / kBK;
   const int64_t hstride = P.ragged ? (int64_t)M : (int64_t)P.rows;  // rows between heads
   const int half = lane >> 5, l32 = lane & 31;
 
@@ -265,8 +276,11 @@ proj_kernel(LayerPlan P, const uint16_t* __restrict__ xt, const uint16_t* __rest
   }
   int dL = blockIdx.x, ds = 0, dm0 = 0, dn0 = 0;  // the next step to load
   if (dL < tiles) tile_of(dL, dm0, dn0);
+  // the LDS byte address of the ring (wave-uniform)
+  const uint32_t lds_addr = (uint32_t)__builtin_amdgcn_readfirstlane(
+      (int)(uint32_t)(uintptr_t)(__attribute__((address_space(3))) void*)lds);
   u32x4_t lrx, lrw;
-  unsigned char* lst;
+  uint32_t lst;
   auto load_prep = [&](int stage) {
     const bool live = dL < tiles;
     const int k0 = ds * kBK;
@@ -274,7 +288,7 @@ proj_kernel(LayerPlan P, const uint16_t* __restrict__ xt, const uint16_t* __rest
     const uint32_t wb = live ? (uint32_t)(((int64_t)(N - dn0) * K - k0) * 2) : 0u;
     lrx = rsrc_sgprs(xt + ((int64_t)dm0 * K + k0), xb);
     lrw = rsrc_sgprs(wp + ((int64_t)dn0 * K + k0), wb);
-    lst = lds + stage * kStageBytes + wave * (kDmaPerTile * 1024);
+    lst = lds_addr + stage * kStageBytes + wave * (kDmaPerTile * 1024);
   };
   auto load_part = [&](int j) {
     dma16(lrx, lst + 1024 * j, loff[j]);
@@ -297,29 +311,41 @@ proj_kernel(LayerPlan P, const uint16_t* __restrict__ xt, const uint16_t* __rest
 #pragma unroll
   for (int ks = 0; ks < 2; ++ks) roff[ks] = tile_off(l32, 2 * ks + half);
   u32x4_t fa[2][TM], fb[2][TN];  // [slice][block]
+  // (the stage's offset passes through an empty asm statement, so that the
+  // addresses are formed at each read rather than held for every stage and
+  // slice, eight registers the epilogue pushed into scratch)
   auto read_slice = [&](int stage, int ks) {
-    const unsigned char* A = lds + stage * kStageBytes + kWaveM * wm * kRowBytes + roff[ks];
-    const unsigned char* B = lds + stage * kStageBytes + kTileBytes + kWaveN * wn * kRowBytes + roff[ks];
+    int so = stage * kStageBytes;
+    asm volatile("" : "+s"(so));
+    const unsigned char* A = lds + so + kWaveM * wm * kRowBytes + roff[ks];
+    const unsigned char* B = lds + so + kTileBytes + kWaveN * wn * kRowBytes + roff[ks];
 #pragma unroll
     for (int i = 0; i < TM; ++i) fa[ks][i] = *reinterpret_cast<const u32x4_t*>(A + 32 * i * kRowBytes);
 #pragma unroll
     for (int j = 0; j < TN; ++j) fb[ks][j] = *reinterpret_cast<const u32x4_t*>(B + 32 * j * kRowBytes);
   };
   f32x16_t acc[TM][TN];
-  auto mfma = [&](int ks, int i, int j) {
+  // FRESH: the tile's first product of this block, accumulating onto zero
+  // (no separate clearing of the 256 accumulator registers)
+  auto mfma = [&](int ks, int i, int j, bool fresh) {
     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, fb[ks][j]),
                                                         __builtin_bit_cast(bf16x8_t, fa[ks][i]),
-                                                        acc[i][j], 0, 0, 0);
+                                                        fresh ? f32x16_t{} : acc[i][j], 0, 0, 0);
   };
 
   // ---- output ----
   // Token row of (head 0, this lane's token m): [B, H, L, .] or [H, T, .].
+  // (The divisor goes through an empty asm statement so that its reciprocal
+  // is formed at each use rather than once before the tile loop, where it
+  // was spilled; a reload's wait would drain the loads in flight.)
   auto token_row = [&](int m) -> int64_t {
     if (P.ragged) return m;
-    const int b = m / P.rows;
-    return (int64_t)b * P.heads * P.rows + (m - b * P.rows);
+    int rows = P.rows;
+    asm volatile("" : "+s"(rows));
+    const int b = m / rows;
+    return (int64_t)b * P.heads * rows + (m - b * rows);
   };
-  // The whole tile at once (every tile without DEFER; gate-logit tiles).
+  // The whole tile at once (every tile without DEFER), eight bytes per lane.
   auto write_now = [&](int m0, int n0) {
     int64_t tokrow[TM];
     bool tok_ok[TM];
@@ -335,9 +361,7 @@ proj_kernel(LayerPlan P, const uint16_t* __restrict__ xt, const uint16_t* __rest
       for (int gq = 0; gq < 4; ++gq) {
         const int nf = n0 + kWaveN * wn + 32 * j + 8 * gq;  // first feature of the group (uniform)
         if (nf >= N) continue;
-        const bool in_proj = nf + 8 <= 4 * Hd;  // else gate logits (4 H d is a multiple of 8)
-        const int blk = in_proj ? nf / Hd : 0, h = in_proj ? (nf % Hd) / P.d : 0;
-        const int e = in_proj ? nf % P.d : 0;
+        const int blk = nf / Hd, h = (nf % Hd) / P.d, e = nf % P.d;
         uint16_t* const dst = blk == 0 ? q : blk == 1 ? k : blk == 2 ? v : r;
         // the group's part of the address, the same for every lane
         unsigned char* const gbase = reinterpret_cast<unsigned char*>(dst) + ((int64_t)h * hstride * P.d + e) * 2;
@@ -346,99 +370,117 @@ proj_kernel(LayerPlan P, const uint16_t* __restrict__ xt, const uint16_t* __rest
           if (!tok_ok[i]) continue;
           const u32x2_t o{pack_bf16x2(acc[i][j][4 * gq], acc[i][j][4 * gq + 1]),
                           pack_bf16x2(acc[i][j][4 * gq + 2], acc[i][j][4 * gq + 3])};
-          if (in_proj) {
-            *reinterpret_cast<u32x2_t*>(gbase + (tokrow[i] * P.d + 4 * half) * 2) = o;
-          } else {
-            for (int f = 0; f < 4; ++f) {
-              const int n = nf + 4 * half + f;
-              if (n < N) a[tokrow[i] + (n - 4 * Hd) * hstride] = (uint16_t)(o[f >> 1] >> (16 * (f & 1)));
-            }
-          }
+          *reinterpret_cast<u32x2_t*>(gbase + (tokrow[i] * P.d + 4 * half) * 2) = o;
         }
       }
     }
   };
   // Deferred output.  At a tile's end each wave stages its 128 x 128 bf16
-  // block, 32 tokens at a time, through the LDS stage of the tile's last
-  // step (rows of 256 bytes, 16-byte chunks XOR-swizzled by the row), and
-  // reads it back as 32 pieces of 16 bytes per lane: piece (i, pass) holds
-  // token 32 i + 4 pass + l / 16 and features 8 (l % 16) .. + 7, so eight
-  // lanes write one token's 128-byte row of a head (d = 64), whole lines.
+  // block, 32 tokens at a time, in LDS as rows of 256 bytes (16-byte chunks
+  // XOR-swizzled by the row) and reads it back as 16-byte pieces: piece
+  // (i, pass) holds token 32 i + 4 pass + l / 16 and features 8 (l % 16) ..
+  // + 7, so eight lanes write one token's 128-byte row of a head (d = 64),
+  // whole lines.  Token block 0 stays in the spare LDS region and is read
+  // piece by piece as its stores go out (the next tile's first eight steps);
+  // blocks 1..3 go through the stage of the tile's last step into registers.
   // The features lie in one of q, k, v, r (H d is a multiple of 256) and the
   // tile's tokens in one sequence or in the packed rows (token rows linear
   // in the token); the targets' extents, tokens * H * d * 2 bytes, are
   // below 2^31 (the launcher checks all three).
   const uint32_t act_bytes = (uint32_t)((int64_t)M * Hd * 2);
-  u32x4_t ob[TM][8];
-  uint32_t obase = 0;   // byte offset of (this lane's first token, its features)
-  int mfirst = 0;       // this lane's first token
-  uint32_t tokstep = 0; // bytes between consecutive tokens' rows
+  u32x4_t ob[TM - 1][8];  // token blocks 1..3 (rotating into ob[0])
+  uint32_t obase = 0;     // byte offset of (this lane's first token, its features)
+  int mfirst = 0;         // this lane's first token
+  uint32_t tokstep = 0;   // bytes between consecutive tokens' rows
   __amdgpu_buffer_rsrc_t rcur = make_rsrc(q, 0u);
   bool ob_live = false;
+  unsigned char* const spare = lds + kStages * kStageBytes + wave * 8192;
   if constexpr (DEFER) {
 #pragma unroll
-    for (int i = 0; i < TM; ++i)
+    for (int i = 0; i + 1 < TM; ++i)
 #pragma unroll
       for (int ps = 0; ps < 8; ++ps) ob[i][ps] = u32x4_t{0u, 0u, 0u, 0u};
   }
+  // byte offset of piece PS in a wave's staged 32-token block
+  auto piece_off = [&](int ps, int el) {
+    const int row = 4 * ps + (el >> 4);
+    return row * 256 + (((el & 15) ^ (row & 15)) * 16);
+  };
   auto defer_tile = [&](int m0, int n0, unsigned char* stage) {
+    const int el = lane_now();
+    const int e32 = el & 31, ehalf = el >> 5;
     unsigned char* const wst = stage + wave * 8192;  // this wave's 32 x 256-byte rows
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
-      // lane (token l32, half) writes features 32 j + 8 gq + 4 half .. + 3
+      unsigned char* const buf = i == 0 ? spare : wst;
+      // lane (token e32, half) writes features 32 j + 8 gq + 4 half .. + 3
+      // (one 32 x 32 block at a time: scheduled freely, the conversions held
+      // enough registers to push the loop's addresses into scratch)
 #pragma unroll
-      for (int j = 0; j < TN; ++j)
+      for (int j = 0; j < TN; ++j) {
 #pragma unroll
         for (int gq = 0; gq < 4; ++gq) {
-          const int ch = (4 * j + gq) ^ (l32 & 15);
-          *reinterpret_cast<u32x2_t*>(wst + l32 * 256 + ch * 16 + 8 * half) =
+          const int ch = (4 * j + gq) ^ (e32 & 15);
+          *reinterpret_cast<u32x2_t*>(buf + e32 * 256 + ch * 16 + 8 * ehalf) =
               u32x2_t{pack_bf16x2(acc[i][j][4 * gq], acc[i][j][4 * gq + 1]),
                       pack_bf16x2(acc[i][j][4 * gq + 2], acc[i][j][4 * gq + 3])};
         }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      if (i == 0) continue;
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
       __builtin_amdgcn_wave_barrier();
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 #pragma unroll
-      for (int ps = 0; ps < 8; ++ps) {
-        const int row = 4 * ps + (lane >> 4);
-        ob[i][ps] = *reinterpret_cast<const u32x4_t*>(wst + row * 256 + (((lane & 15) ^ (row & 15)) * 16));
-      }
+      for (int ps = 0; ps < 8; ++ps) ob[i - 1][ps] = *reinterpret_cast<const u32x4_t*>(wst + piece_off(ps, el));
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
       __builtin_amdgcn_wave_barrier();
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     }
-    const int nf = n0 + kWaveN * wn, blk = nf / Hd;
-    const int c = nf % Hd + 8 * (lane & 15), h = c / P.d, e = c % P.d;
+    int hd = Hd, dd = P.d;
+    asm volatile("" : "+s"(hd), "+s"(dd));
+    const int nf = n0 + kWaveN * wn, blk = nf / hd;
+    const int c = nf % hd + 8 * (el & 15), h = c / dd, e = c % dd;
     uint16_t* const dst = blk == 0 ? q : blk == 1 ? k : blk == 2 ? v : r;
     rcur = make_rsrc(dst, act_bytes);
-    mfirst = m0 + kWaveM * wm + (lane >> 4);
+    mfirst = m0 + kWaveM * wm + (el >> 4);
     obase = (uint32_t)(((token_row(mfirst) + (int64_t)h * hstride) * P.d + e) * 2);
     tokstep = (uint32_t)(P.d * 2);
   };
-  // Store PS of token block SB (its pieces rotate into ob[0], one block per
-  // eight steps); nothing pending past the fourth block.
-  auto store_slot = [&](auto ps_c, int sb) {
-    constexpr int ps = decltype(ps_c)::value;
+  // Store piece PS of token block SB, DATA; nothing pending past the fourth
+  // block.
+  auto store_piece = [&](const u32x4_t& data, int ps, int sb) {
     const int dm = 32 * sb + 4 * ps;
     const bool live = ob_live && sb < TM && mfirst + dm < M;
-    __builtin_amdgcn_raw_buffer_store_b128(ob[0][ps], rcur, live ? obase + dm * tokstep : kOutOfRange, 0, 0);
+    __builtin_amdgcn_raw_buffer_store_b128(data, rcur, live ? obase + dm * tokstep : kOutOfRange, 0, 0);
+  };
+  auto spare_piece = [&](int ps) {  // piece PS of token block 0
+    return *reinterpret_cast<const u32x4_t*>(spare + piece_off(ps, lane_now()));
   };
 
   // ---- one K step ----
   // With DEFER, steps come in blocks of eight from a step that is a multiple
   // of 8, so step gg's stage is u % 4.
-  auto step = [&](int gg, auto u_c, int sb) {
+  // BLK0: the tile's first block of eight steps (its stores read block 0 from
+  // the spare region).
+  auto step = [&](int gg, auto u_c, int sb, auto first_c, auto blk0_c) {
     constexpr int u = decltype(u_c)::value;
+    constexpr bool fresh = decltype(first_c)::value && u == 0;  // the tile's first step
+    constexpr bool blk0 = decltype(blk0_c)::value;
     const int st = DEFER ? (u & (kStages - 1)) : (gg & (kStages - 1));
     wait_vm<2 * kDmaPerTile + (DEFER ? 2 * kStoresPerStep : 0)>();  // own loads of step gg + 1 in
     step_sync();  // everyone's; the stage of step gg - 1 is free
-    load_prep((st + 3) & (kStages - 1));
     read_slice(st, 1);
+    u32x4_t sp{};
+    if constexpr (DEFER && blk0) sp = spare_piece(u);
     __builtin_amdgcn_sched_barrier(0);
+    // slice-0 products, a pair of loads after each row (the descriptors formed
+    // under the first row)
 #pragma unroll
-    for (int i = 0; i < TM; ++i) {  // slice-0 products, a pair of loads after each row
+    for (int i = 0; i < TM; ++i) {
 #pragma unroll
-      for (int j = 0; j < TN; ++j) mfma(0, i, j);
+      for (int j = 0; j < TN; ++j) mfma(0, i, j, fresh);
+      if (i == 0) load_prep((st + 3) & (kStages - 1));
       __builtin_amdgcn_sched_barrier(0);
       load_part(i);
       __builtin_amdgcn_sched_barrier(0);
@@ -451,11 +493,14 @@ proj_kernel(LayerPlan P, const uint16_t* __restrict__ xt, const uint16_t* __rest
 #pragma unroll
       for (int i = 2 * hh; i < 2 * hh + 2; ++i)
 #pragma unroll
-        for (int j = 0; j < TN; ++j) mfma(1, i, j);
+        for (int j = 0; j < TN; ++j) mfma(1, i, j, false);
       if constexpr (DEFER) {
         if (hh == 0) {
           __builtin_amdgcn_sched_barrier(0);
-          store_slot(u_c, sb);
+          if constexpr (blk0)
+            store_piece(sp, u, 0);
+          else
+            store_piece(ob[0][u], u, sb);
           __builtin_amdgcn_sched_barrier(0);
         }
       }
@@ -470,7 +515,7 @@ proj_kernel(LayerPlan P, const uint16_t* __restrict__ xt, const uint16_t* __rest
 #pragma unroll
     for (int j = 0; j < kDmaPerTile; ++j) load_part(j);
     load_advance();
-    if constexpr (DEFER) store_slot(std::integral_constant<int, 0>{}, TM);  // placeholder
+    if constexpr (DEFER) store_piece(ob[0][0], 0, TM);  // placeholder
   }
   wait_vm<2 * (2 * kDmaPerTile + (DEFER ? 2 * kStoresPerStep : 0))>();
   step_sync();
@@ -480,49 +525,105 @@ proj_kernel(LayerPlan P, const uint16_t* __restrict__ xt, const uint16_t* __rest
   for (int L = blockIdx.x; L < tiles; L += gridDim.x) {
     int m0, n0;
     tile_of(L, m0, n0);
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-      for (int j = 0; j < TN; ++j)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
     if constexpr (DEFER) {
-      for (int s = 0, sb = 0; s < nk; s += 8, ++sb) {
-        unrolled(std::make_integer_sequence<int, 8>{}, [&](auto u_c) { step(g + decltype(u_c)::value, u_c, sb); });
+      // the first block of eight steps, its first step accumulating onto zero
+      step(g, std::integral_constant<int, 0>{}, 0, std::true_type{}, std::true_type{});
+      unrolled(std::make_integer_sequence<int, 7>{}, [&](auto v_c) {
+        step(g + decltype(v_c)::value + 1, std::integral_constant<int, decltype(v_c)::value + 1>{}, 0,
+             std::false_type{}, std::true_type{});
+      });
+      g += 8;
+      for (int s = 8, sb = 1; s < nk; s += 8, ++sb) {
+        unrolled(std::make_integer_sequence<int, 8>{},
+                 [&](auto u_c) { step(g + decltype(u_c)::value, u_c, sb, std::false_type{}, std::false_type{}); });
         g += 8;
 #pragma unroll
-        for (int i = 0; i + 1 < TM; ++i)  // the next token block's pieces
+        for (int i = 0; i + 2 < TM; ++i)  // the next token block's pieces
 #pragma unroll
           for (int ps = 0; ps < 8; ++ps) ob[i][ps] = ob[i + 1][ps];
       }
-      if (n0 >= 4 * Hd) {  // gate logits (the last feature tile)
-        write_now(m0, n0);
-        wait_vm<0>();  // the variable number of stores drained: the counts stay exact
-        ob_live = false;
-      } else {
-        step_sync();  // every wave done reading the stage of the tile's last step
-        defer_tile(m0, n0, lds + ((g - 1) & (kStages - 1)) * kStageBytes);
-        ob_live = true;
-      }
+      step_sync();  // every wave done reading the stage of the tile's last step
+      defer_tile(m0, n0, lds + ((g - 1) & (kStages - 1)) * kStageBytes);
+      ob_live = true;
     } else {
-      for (int s = 0; s < nk; ++s, ++g) step(g, std::integral_constant<int, 0>{}, 0);
+      step(g++, std::integral_constant<int, 0>{}, 0, std::true_type{}, std::false_type{});
+      for (int s = 1; s < nk; ++s, ++g)
+        step(g, std::integral_constant<int, 0>{}, 0, std::false_type{}, std::false_type{});
       write_now(m0, n0);
     }
   }
   if constexpr (DEFER) {  // the last tile's stores
     if (ob_live) {
-      for (int sb = 0; sb < TM; ++sb) {
-        unrolled(std::make_integer_sequence<int, 8>{}, [&](auto ps_c) { store_slot(ps_c, sb); });
+      unrolled(std::make_integer_sequence<int, 8>{},
+               [&](auto ps_c) { store_piece(spare_piece(decltype(ps_c)::value), decltype(ps_c)::value, 0); });
 #pragma unroll
-        for (int i = 0; i + 1 < TM; ++i)
+      for (int sb = 1; sb < TM; ++sb)
 #pragma unroll
-          for (int ps = 0; ps < 8; ++ps) ob[i][ps] = ob[i + 1][ps];
-      }
+        for (int ps = 0; ps < 8; ++ps) store_piece(ob[sb - 1][ps], ps, sb);
     }
   }
   // drain: every load into LDS (the steps past the last tile read zeros)
   // has landed before the workgroup ends
   wait_vm<0>();
+}
+
+// ---------------------------------------------------------------------------
+// gate_kernel: the gate logits a = Xt w_g^T (the last H rows of Wp), rounded
+// to bf16, in the [B, H, L] / [H, T] layout.  H outputs per token make this a
+// pass over Xt rather than a GEMM tile: in the projection kernel they would
+// fill a 256-feature tile for 16 features.  A wave takes 32 tokens and up to
+// 32 gates per pass on v_mfma_f32_32x32x16_bf16 with the gate rows as the
+// first operand, so lane l holds token l % 32 (32 consecutive tokens of one
+// gate row per store).  The products may sum the model channels in any
+// order that pairs Xt and w_g alike: lane half h of product u takes
+// channels k + 32 h + 8 u .. + 7, so each lane reads 64 contiguous bytes of
+// its row per four products.
+// ---------------------------------------------------------------------------
+constexpr int kGateTokens = 128;  // per workgroup (4 waves of 32)
+
+__global__ void __launch_bounds__(kThreads)
+gate_kernel(LayerPlan P, const uint16_t* __restrict__ xt, const uint16_t* __restrict__ wp,
+            uint16_t* __restrict__ a) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int l32 = lane & 31, half = lane >> 5;
+  const int K = P.d_model, M = P.tokens, H = P.heads;
+  const int t0 = blockIdx.x * kGateTokens + 32 * wave;
+  if (t0 >= M) return;  // no barrier follows
+  const int64_t grow0 = (int64_t)4 * H * P.d;  // first gate row of Wp
+  const __amdgpu_buffer_rsrc_t rx = make_rsrc(xt, (uint32_t)((int64_t)M * K * 2));
+  const __amdgpu_buffer_rsrc_t rw = make_rsrc(wp + grow0 * K, (uint32_t)((int64_t)H * K * 2));
+  const int m = t0 + l32;
+  int64_t arow = m;  // row of (gate 0, token m) in a
+  if (!P.ragged) {
+    const int b = m / P.rows;
+    arow = (int64_t)b * H * P.rows + (m - b * P.rows);
+  }
+  const int64_t hstride = P.ragged ? (int64_t)M : (int64_t)P.rows;
+  // rows past the last token (gate) read zeros: their offsets pass the extent
+  const uint32_t xo = ((uint32_t)m * (uint32_t)K + 32u * half) * 2u;
+  for (int g0 = 0; g0 < H; g0 += 32) {
+    const uint32_t wo = ((uint32_t)(g0 + l32) * (uint32_t)K + 32u * half) * 2u;
+    f32x16_t acc = {};
+    for (int k0 = 0; k0 < K; k0 += 64) {
+      u32x4_t xa[4], wa[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        xa[u] = bload(rx, xo + (uint32_t)(k0 + 8 * u) * 2u);
+        wa[u] = bload(rw, wo + (uint32_t)(k0 + 8 * u) * 2u);
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, wa[u]),
+                                                      __builtin_bit_cast(bf16x8_t, xa[u]), acc, 0, 0, 0);
+    }
+    if (m < M) {
+#pragma unroll
+      for (int rr = 0; rr < 16; ++rr) {
+        const int gi = g0 + 8 * (rr >> 2) + 4 * half + (rr & 3);
+        if (gi < H) a[arow + gi * hstride] = (uint16_t)pack_bf16x2(acc[rr], 0.0f);
+      }
+    }
+  }
 }
 
 }  // namespace
@@ -531,7 +632,7 @@ gbla_status launch_project(const LayerPlan& p, const void* x, const float* conv_
                            const void* w_proj, const int32_t* cu, void* xt, void* q, void* k,
                            void* v, void* r, void* a, hipStream_t st) {
   if (p.tokens == 0) return GBLA_OK;
-  const int64_t tiles = (int64_t)((p.features + kBN - 1) / kBN) * ((p.tokens + kBM - 1) / kBM);
+  const int64_t tiles = (int64_t)((4 * p.heads * p.d + kBN - 1) / kBN) * ((p.tokens + kBM - 1) / kBM);
   if (tiles > 2147483647LL) return GBLA_ERR_UNSUPPORTED;  // the grid's x extent; nothing enqueued
   hipLaunchKernelGGL(conv_x_kernel, dim3((p.d_model + 127) / 128, (p.tokens + 16 * kConvRun - 1) / (16 * kConvRun)),
                      dim3(kThreads), 0, st, p, (const uint16_t*)x, conv_x, cu, (uint16_t*)xt);
@@ -545,7 +646,9 @@ gbla_status launch_project(const LayerPlan& p, const void* x, const float* conv_
                      (int64_t)p.tokens * p.heads * p.d * 2 < (int64_t(1) << 31);
   hipLaunchKernelGGL(defer ? proj_kernel<true> : proj_kernel<false>, grid, dim3(kProjThreads), 0, st, p,
                      (const uint16_t*)xt, (const uint16_t*)w_proj, (uint16_t*)q, (uint16_t*)k,
-                     (uint16_t*)v, (uint16_t*)r, (uint16_t*)a);
+                     (uint16_t*)v, (uint16_t*)r);
+  hipLaunchKernelGGL(gate_kernel, dim3((unsigned)((p.tokens + kGateTokens - 1) / kGateTokens)), dim3(kThreads), 0,
+                     st, p, (const uint16_t*)xt, (const uint16_t*)w_proj, (uint16_t*)a);
   return hipGetLastError() == hipSuccess ? GBLA_OK : GBLA_ERR_HIP;
 }
 
