@@ -571,52 +571,93 @@ proj_kernel(LayerPlan P, const uint16_t* __restrict__ xt, const uint16_t* __rest
 // gate_kernel: the gate logits a = Xt w_g^T (the last H rows of Wp), rounded
 // to bf16, in the [B, H, L] / [H, T] layout.  H outputs per token make this a
 // pass over Xt rather than a GEMM tile: in the projection kernel they would
-// fill a 256-feature tile for 16 features.  A wave takes 32 tokens and up to
-// 32 gates per pass on v_mfma_f32_32x32x16_bf16 with the gate rows as the
-// first operand, so lane l holds token l % 32 (32 consecutive tokens of one
-// gate row per store).  The products may sum the model channels in any
-// order that pairs Xt and w_g alike: lane half h of product u takes
-// channels k + 32 h + 8 u .. + 7, so each lane reads 64 contiguous bytes of
-// its row per four products.
+// fill a 256-feature tile for 16 features.  A workgroup takes 128 tokens; per
+// step of 128 model channels its threads load the 128 x 256-byte slab with
+// 16 lanes to a row (whole lines; one lane per row, as the MFMA operand
+// layout would have it, cost an L2 request per 16 bytes), store it to LDS
+// (16-byte chunks XOR-swizzled by the row), together with the same channels
+// of up to 32 gate rows, and each wave multiplies its 32 tokens by the gates
+// on v_mfma_f32_32x32x16_bf16, the gate rows as the first operand: lane l
+// holds token l % 32, so a gate's 32 consecutive tokens are written
+// together.  The next step's slabs are loaded into registers while the
+// current ones are multiplied, into one LDS buffer of 40 KB (a second
+// buffer, or W read through the cache, measured no faster).
 // ---------------------------------------------------------------------------
 constexpr int kGateTokens = 128;  // per workgroup (4 waves of 32)
 
 __global__ void __launch_bounds__(kThreads)
 gate_kernel(LayerPlan P, const uint16_t* __restrict__ xt, const uint16_t* __restrict__ wp,
             uint16_t* __restrict__ a) {
+  __shared__ __attribute__((aligned(16))) unsigned char slab[kGateTokens * 256];
+  __shared__ __attribute__((aligned(16))) unsigned char wslab[32 * 256];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l32 = lane & 31, half = lane >> 5;
   const int K = P.d_model, M = P.tokens, H = P.heads;
-  const int t0 = blockIdx.x * kGateTokens + 32 * wave;
-  if (t0 >= M) return;  // no barrier follows
+  const int tb = blockIdx.x * kGateTokens;
   const int64_t grow0 = (int64_t)4 * H * P.d;  // first gate row of Wp
+  // rows past the last token (gate) read zeros: their offsets pass the extent
   const __amdgpu_buffer_rsrc_t rx = make_rsrc(xt, (uint32_t)((int64_t)M * K * 2));
   const __amdgpu_buffer_rsrc_t rw = make_rsrc(wp + grow0 * K, (uint32_t)((int64_t)H * K * 2));
-  const int m = t0 + l32;
-  int64_t arow = m;  // row of (gate 0, token m) in a
-  if (!P.ragged) {
-    const int b = m / P.rows;
-    arow = (int64_t)b * H * P.rows + (m - b * P.rows);
-  }
-  const int64_t hstride = P.ragged ? (int64_t)M : (int64_t)P.rows;
-  // rows past the last token (gate) read zeros: their offsets pass the extent
-  const uint32_t xo = ((uint32_t)m * (uint32_t)K + 32u * half) * 2u;
-  for (int g0 = 0; g0 < H; g0 += 32) {
-    const uint32_t wo = ((uint32_t)(g0 + l32) * (uint32_t)K + 32u * half) * 2u;
-    f32x16_t acc = {};
-    for (int k0 = 0; k0 < K; k0 += 64) {
-      u32x4_t xa[4], wa[4];
+  // slab loads: thread t takes chunk t % 16 of rows t / 16 + 16 j
+  const int lc = tid & 15, lr = tid >> 4;
+  auto load = [&](int k0, int g0, u32x4_t (&x)[10]) {
+    const bool in = k0 + 8 * lc < K;
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        xa[u] = bload(rx, xo + (uint32_t)(k0 + 8 * u) * 2u);
-        wa[u] = bload(rw, wo + (uint32_t)(k0 + 8 * u) * 2u);
+    for (int j = 0; j < 8; ++j)
+      x[j] = bload(rx, in ? ((uint32_t)(tb + lr + 16 * j) * (uint32_t)K + (uint32_t)(k0 + 8 * lc)) * 2u : kOutOfRange);
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+      x[8 + j] = bload(rw, in ? ((uint32_t)(g0 + lr + 16 * j) * (uint32_t)K + (uint32_t)(k0 + 8 * lc)) * 2u : kOutOfRange);
+  };
+  auto put = [&](const u32x4_t (&x)[10]) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int row = lr + 16 * j;
+      *reinterpret_cast<u32x4_t*>(&slab[row * 256 + ((lc ^ (row & 15)) << 4)]) = x[j];
+    }
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int row = lr + 16 * j;
+      *reinterpret_cast<u32x4_t*>(&wslab[row * 256 + ((lc ^ (row & 15)) << 4)]) = x[8 + j];
+    }
+  };
+  const int m = tb + 32 * wave + l32;  // this lane's token in the products
+  const int srow = 32 * wave + l32;
+  // d_model is a multiple of 64: the last step may be half empty, its
+  // channels past d_model read as zeros (out-of-range offsets)
+  const int nk = (K + 127) / 128;
+  for (int g0 = 0; g0 < H; g0 += 32) {
+    f32x16_t acc = {};
+    u32x4_t x[10];
+    load(0, g0, x);
+    put(x);
+    __syncthreads();
+    for (int s = 0; s < nk; ++s) {
+      if (s + 1 < nk) load(128 * (s + 1), g0, x);
+      u32x4_t wa[8], xa[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int ch = 2 * u + half;
+        wa[u] = *reinterpret_cast<const u32x4_t*>(&wslab[l32 * 256 + ((ch ^ (l32 & 15)) << 4)]);
+        xa[u] = *reinterpret_cast<const u32x4_t*>(&slab[srow * 256 + ((ch ^ (srow & 15)) << 4)]);
       }
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
+      for (int u = 0; u < 8; ++u)
         acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, wa[u]),
                                                       __builtin_bit_cast(bf16x8_t, xa[u]), acc, 0, 0, 0);
+      __syncthreads();  // every wave done reading the slabs
+      if (s + 1 < nk) {
+        put(x);
+        __syncthreads();
+      }
     }
     if (m < M) {
+      int64_t arow = m;  // row of (gate 0, token m) in a
+      if (!P.ragged) {
+        const int b = m / P.rows;
+        arow = (int64_t)b * H * P.rows + (m - b * P.rows);
+      }
+      const int64_t hstride = P.ragged ? (int64_t)M : (int64_t)P.rows;
 #pragma unroll
       for (int rr = 0; rr < 16; ++rr) {
         const int gi = g0 + 8 * (rr >> 2) + 4 * half + (rr & 3);
