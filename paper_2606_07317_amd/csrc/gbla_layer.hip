@@ -6,9 +6,9 @@
 // proj_kernel    P = Xt Wp^T on v_mfma_f32_32x32x16_bf16 (fp32 accumulation):
 //                a workgroup of 4 waves (2 x 2, 128 x 128 each, one per
 //                SIMD, accumulators in AGPRs) computes a 256-token x
-//                256-feature tile, 32 model channels per K step, the
-//                operand rows loaded straight into a four-step LDS ring
-//                three steps ahead.  The output is rounded to bf16 and
+//                256-feature tile, 64 model channels per K step, the
+//                operand rows loaded straight into a two-step LDS ring one
+//                step ahead.  The output is rounded to bf16 and
 //                scattered to the head-major layout the attention kernels
 //                read ([B, H, n, d] / [B, H, n]), written under the next
 //                tile's products where the shape allows.
@@ -29,13 +29,13 @@
 namespace gbla {
 namespace {
 
-constexpr int kBM = 256, kBN = 256, kBK = 32;
+constexpr int kBM = 256, kBN = 256, kBK = 64;
 constexpr int kProjWaves = 4, kProjThreads = 64 * kProjWaves;  // 2 x 2 waves
 constexpr int kProjGrid = 256;                                  // persistent workgroups
 constexpr int kWaveM = kBM / 2, kWaveN = kBN / 2;               // 128 x 128 per wave
-constexpr int kRowBytes = kBK * 2;           // one tile row of bf16: four 16-byte chunks
-constexpr int kTileBytes = 256 * kRowBytes;  // 16 KB
-constexpr int kStages = 4;                   // K steps held in LDS at once
+constexpr int kRowBytes = kBK * 2;           // one tile row of bf16: eight 16-byte chunks
+constexpr int kTileBytes = 256 * kRowBytes;  // 32 KB
+constexpr int kStages = 2;                   // K steps held in LDS at once
 constexpr int kStageBytes = 2 * kTileBytes;  // both tiles of one K step
 // the ring, then a spare 32 KB: one 32-token block of every wave's staged
 // output (the deferred stores' first eight)
@@ -44,12 +44,12 @@ constexpr int kLdsBytes = kStages * kStageBytes + kSpareBytes;
 // per wave and K step: 16-byte loads into LDS, 1 KB (64 lanes) each
 constexpr int kDmaPerTile = kTileBytes / (kProjThreads * 16);
 
-// Byte offset of 16-byte chunk `c` of row `r` in a tile.  The chunks are
-// XOR-swizzled by r / 4: a 16-byte operand read serves 16 lanes (16
-// consecutive rows) per cycle from 64 banks (256 bytes), and four rows share
-// a 256-byte bank row, so the four rows of a bank row take its four chunks
-// and the swizzle gives the four groups of four rows different chunks.
-__device__ __forceinline__ int tile_off(int r, int c) { return r * kRowBytes + ((c ^ ((r >> 2) & 3)) << 4); }
+// Byte offset of 16-byte chunk `c` of row `r` in a tile (128-byte rows, eight
+// chunks).  The chunks are XOR-swizzled by r % 8: a 16-byte operand read
+// serves 16 lanes (16 consecutive rows) from 64 banks (256 bytes, two rows),
+// and the swizzle gives the even rows, and the odd rows, of each group of
+// eight different chunks.
+__device__ __forceinline__ int tile_off(int r, int c) { return r * kRowBytes + ((c ^ (r & 7)) << 4); }
 
 // A buffer resource over `bytes` bytes from `base`, as four scalar registers
 // for the assembly loads below (the same descriptor as make_rsrc).
@@ -80,6 +80,9 @@ __device__ __forceinline__ int lane_now() {
   asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(l));
   return l;
 }
+
+// s_waitcnt lgkmcnt(0), the other counters left alone (gfx9 encoding).
+__device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(0xC07F); }
 
 // s_waitcnt vmcnt(N), the other counters left alone (gfx9 encoding).
 template <int N>
@@ -188,31 +191,30 @@ conv_x_kernel(LayerPlan P, const uint16_t* __restrict__ x, const float* __restri
 // AGPRs, and a 128 x 128 wave tile reads 0.5 KB of LDS operands per
 // 32x32x16 product.
 //
-// The K steps of all the workgroup's tiles form one stream, numbered g:
-// step g sits in LDS stage g % 4, loaded by buffer loads that write LDS
-// directly (no staging registers, no LDS stores) three steps ahead.  At the
-// top of step g every wave waits for its own loads of step g + 1 and the
-// workgroup meets at a barrier; the loads of step g + 3 then refill the
-// stage of step g - 1, issued between the step's first products.  A wave
-// reads its slice-1 operands of step g and its slice-0 operands of step
-// g + 1 while the products of the step run, so the products after a
-// barrier never wait for LDS.
+// The K steps (64 channels) of all the workgroup's tiles form one stream,
+// numbered g: step g sits in LDS stage g % 2, loaded by buffer loads that
+// write LDS directly (no staging registers, no LDS stores) one step ahead.
+// At the top of step g every wave waits for its own loads of step g and the
+// workgroup meets at a barrier; the loads of step g + 1 then refill the
+// stage of step g - 1, issued between the step's first products.  Eight
+// lanes load a row's 128 bytes, whole lines: with 32-channel steps (64
+// bytes a row, a four-stage ring three steps ahead) every line took two L2
+// requests, and the kernel ran 3% slower.  Within a step, each of the four
+// 16-channel slices is read while the previous slice's products run.
 //
 // Output: the products are formed as P^T (Wp rows as the first operand),
 // so lane l of a 32 x 32 block holds token l % 32 and, in elements
 // 4 g .. 4 g + 3, the four consecutive features 8 g + 4 (l / 32) .. + 3.
 // Stores must cover whole lines: 16 bytes per lane at different tokens'
 // rows cost an L2 request each, which made the output as slow as the
-// products.  So with DEFER (d_model a multiple of 1024, i.e. at least 32 K
+// products.  So with DEFER (d_model a multiple of 1024, i.e. at least 16 K
 // steps per tile; a tile's features in one of q, k, v, r; its tokens' rows
 // linear) each wave stages its block through LDS at the tile's end and
 // reads it back as 16-byte pieces, eight lanes to a 128-byte row, which go
-// out one per K step of the next tile, under its products.  Every step then
-// issues exactly one store (to an out-of-range offset when none is
-// pending), so the load waits keep exact counts.  Without DEFER, and for
-// the tile holding the gate logits (destinations H rows apart, written one
-// by one), the tile is written from the accumulators at once (eight bytes
-// per lane) and, with DEFER, drained.
+// out two per K step of the next tile, under its products (to an
+// out-of-range offset when none is pending), ahead of the step's loads.
+// Without DEFER the tile is written from the accumulators at once (eight
+// bytes per lane).
 //
 // The dispatcher places workgroup b on XCD b % 8; with a grid that is a
 // multiple of 8, tile L therefore runs on XCD L % 8.  When the token tiles
@@ -233,7 +235,7 @@ proj_kernel(LayerPlan P, const uint16_t* __restrict__ xt, const uint16_t* __rest
             uint16_t* __restrict__ r) {
   __shared__ __attribute__((aligned(1024))) unsigned char lds[kLdsBytes];
   constexpr int TM = kWaveM / 32, TN = kWaveN / 32;  // 32 x 32 products per wave and K slice
-  constexpr int kStoresPerStep = 1;  // deferred 16-byte stores per lane and K step
+  constexpr int kStoresPerStep = 2;  // deferred 16-byte stores per lane and K step
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;
@@ -261,19 +263,16 @@ proj_kernel(LayerPlan P, const uint16_t* __restrict__ xt, const uint16_t* __rest
   const int half = lane >> 5, l32 = lane & 31;
 
   // ---- the load stream ----
-  // Load j of a wave covers tile rows 16 (kDmaPerTile wave + j) .. + 15: lane
-  // l writes row (l / 4), stored chunk l % 4, which holds source chunk
-  // (l % 4) ^ (row / 4 % 4) (the swizzle of tile_off).  The offsets within the
+  // Load j of a wave covers tile rows 8 (kDmaPerTile wave + j) .. + 7: lane
+  // l writes row (l / 8), stored chunk l % 8, which holds source chunk
+  // (l % 8) ^ (row % 8) (the swizzle of tile_off).  The offsets within the
   // tile are the same for Xt and Wp; the tile's first row and the K step go
   // into the descriptor, whose extent ends at the last token (feature), so
   // rows past it read zeros.
-  uint32_t loff[kDmaPerTile];
-#pragma unroll
-  for (int j = 0; j < kDmaPerTile; ++j) {
-    const int row = 16 * (kDmaPerTile * wave + j) + (lane >> 2);
-    const int ch = (lane & 3) ^ ((lane >> 4) & 3);
-    loff[j] = (uint32_t)(row * K + 8 * ch) * 2u;
-  }
+  // the lane's part of the offsets (row lane / 8, its source chunk); each
+  // load adds its first row through an opaque row pitch, so that the eight
+  // sums are formed at the loads rather than held in registers
+  const uint32_t lbase = (uint32_t)(((lane >> 3) * K + 8 * ((lane & 7) ^ ((lane >> 3) & 7))) * 2);
   int dL = blockIdx.x, ds = 0, dm0 = 0, dn0 = 0;  // the next step to load
   if (dL < tiles) tile_of(dL, dm0, dn0);
   // the LDS byte address of the ring (wave-uniform)
@@ -291,8 +290,11 @@ proj_kernel(LayerPlan P, const uint16_t* __restrict__ xt, const uint16_t* __rest
     lst = lds_addr + stage * kStageBytes + wave * (kDmaPerTile * 1024);
   };
   auto load_part = [&](int j) {
-    dma16(lrx, lst + 1024 * j, loff[j]);
-    dma16(lrw, lst + kTileBytes + 1024 * j, loff[j]);
+    int pitch = 2 * K;
+    asm volatile("" : "+s"(pitch));
+    const uint32_t off = lbase + (uint32_t)(8 * (kDmaPerTile * wave + j) * pitch);
+    dma16(lrx, lst + 1024 * j, off);
+    dma16(lrw, lst + kTileBytes + 1024 * j, off);
   };
   auto load_advance = [&]() {
     if (++ds == nk) {
@@ -307,10 +309,10 @@ proj_kernel(LayerPlan P, const uint16_t* __restrict__ xt, const uint16_t* __rest
   // 2 ks + l / 32.  Blocks start at multiples of 32 rows, so the swizzle
   // depends on the lane only: one offset per slice, the block and stage
   // added.
-  int roff[2];
+  int roff[4];
 #pragma unroll
-  for (int ks = 0; ks < 2; ++ks) roff[ks] = tile_off(l32, 2 * ks + half);
-  u32x4_t fa[2][TM], fb[2][TN];  // [slice][block]
+  for (int ks = 0; ks < 4; ++ks) roff[ks] = tile_off(l32, 2 * ks + half);
+  u32x4_t fa[2][TM], fb[2][TN];  // [slice % 2][block]
   // (the stage's offset passes through an empty asm statement, so that the
   // addresses are formed at each read rather than held for every stage and
   // slice, eight registers the epilogue pushed into scratch)
@@ -320,16 +322,16 @@ proj_kernel(LayerPlan P, const uint16_t* __restrict__ xt, const uint16_t* __rest
     const unsigned char* A = lds + so + kWaveM * wm * kRowBytes + roff[ks];
     const unsigned char* B = lds + so + kTileBytes + kWaveN * wn * kRowBytes + roff[ks];
 #pragma unroll
-    for (int i = 0; i < TM; ++i) fa[ks][i] = *reinterpret_cast<const u32x4_t*>(A + 32 * i * kRowBytes);
+    for (int i = 0; i < TM; ++i) fa[ks & 1][i] = *reinterpret_cast<const u32x4_t*>(A + 32 * i * kRowBytes);
 #pragma unroll
-    for (int j = 0; j < TN; ++j) fb[ks][j] = *reinterpret_cast<const u32x4_t*>(B + 32 * j * kRowBytes);
+    for (int j = 0; j < TN; ++j) fb[ks & 1][j] = *reinterpret_cast<const u32x4_t*>(B + 32 * j * kRowBytes);
   };
   f32x16_t acc[TM][TN];
   // FRESH: the tile's first product of this block, accumulating onto zero
   // (no separate clearing of the 256 accumulator registers)
   auto mfma = [&](int ks, int i, int j, bool fresh) {
-    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, fb[ks][j]),
-                                                        __builtin_bit_cast(bf16x8_t, fa[ks][i]),
+    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, fb[ks & 1][j]),
+                                                        __builtin_bit_cast(bf16x8_t, fa[ks & 1][i]),
                                                         fresh ? f32x16_t{} : acc[i][j], 0, 0, 0);
   };
 
@@ -381,7 +383,7 @@ proj_kernel(LayerPlan P, const uint16_t* __restrict__ xt, const uint16_t* __rest
   // (i, pass) holds token 32 i + 4 pass + l / 16 and features 8 (l % 16) ..
   // + 7, so eight lanes write one token's 128-byte row of a head (d = 64),
   // whole lines.  Token block 0 stays in the spare LDS region and is read
-  // piece by piece as its stores go out (the next tile's first eight steps);
+  // piece by piece as its stores go out (the next tile's first four steps);
   // blocks 1..3 go through the stage of the tile's last step into registers.
   // The features lie in one of q, k, v, r (H d is a multiple of 256) and the
   // tile's tokens in one sequence or in the packed rows (token rows linear
@@ -437,6 +439,11 @@ proj_kernel(LayerPlan P, const uint16_t* __restrict__ xt, const uint16_t* __rest
       __builtin_amdgcn_wave_barrier();
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     }
+    // The staging's LDS writes and read-backs complete before the next step's
+    // barrier, after which another wave's loads refill this stage (the
+    // read-backs' results are used only later, by the stores, so nothing
+    // else would wait for them).
+    wait_lgkm0();
     int hd = Hd, dd = P.d;
     asm volatile("" : "+s"(hd), "+s"(dd));
     const int nf = n0 + kWaveN * wn, blk = nf / hd;
@@ -459,84 +466,84 @@ proj_kernel(LayerPlan P, const uint16_t* __restrict__ xt, const uint16_t* __rest
   };
 
   // ---- one K step ----
-  // With DEFER, steps come in blocks of eight from a step that is a multiple
-  // of 8, so step gg's stage is u % 4.
-  // BLK0: the tile's first block of eight steps (its stores read block 0 from
+  // With DEFER, steps come in blocks of four from a step that is a multiple
+  // of 4, so step gg's stage is u % 2.
+  // BLK0: the tile's first block of four steps (its stores read block 0 from
   // the spare region).
   auto step = [&](int gg, auto u_c, int sb, auto first_c, auto blk0_c) {
     constexpr int u = decltype(u_c)::value;
     constexpr bool fresh = decltype(first_c)::value && u == 0;  // the tile's first step
     constexpr bool blk0 = decltype(blk0_c)::value;
     const int st = DEFER ? (u & (kStages - 1)) : (gg & (kStages - 1));
-    wait_vm<2 * kDmaPerTile + (DEFER ? 2 * kStoresPerStep : 0)>();  // own loads of step gg + 1 in
+    // Own loads of step gg in.  Everything in flight is waited for: loads and
+    // stores share the counter and need not complete in order, so a count
+    // that leaves the last stores out would not prove the loads complete.
+    // The step's stores therefore go out before its loads, under its first
+    // products, and have a whole step to finish.
+    wait_vm<0>();
     step_sync();  // everyone's; the stage of step gg - 1 is free
-    read_slice(st, 1);
-    u32x4_t sp{};
-    if constexpr (DEFER && blk0) sp = spare_piece(u);
-    __builtin_amdgcn_sched_barrier(0);
-    // slice-0 products, a pair of loads after each row (the descriptors formed
-    // under the first row)
-#pragma unroll
-    for (int i = 0; i < TM; ++i) {
-#pragma unroll
-      for (int j = 0; j < TN; ++j) mfma(0, i, j, fresh);
-      if (i == 0) load_prep((st + 3) & (kStages - 1));
-      __builtin_amdgcn_sched_barrier(0);
-      load_part(i);
-      __builtin_amdgcn_sched_barrier(0);
+    read_slice(st, 0);
+    u32x4_t sp[2] = {};
+    if constexpr (DEFER && blk0) {
+      sp[0] = spare_piece(2 * u);
+      sp[1] = spare_piece(2 * u + 1);
     }
-    load_advance();
-    read_slice((st + 1) & (kStages - 1), 0);  // the next step's (next tile's) first slice
-    // slice-1 products, the deferred store after the first half
+    load_prep((st + 1) & (kStages - 1));
+    __builtin_amdgcn_sched_barrier(0);
+    // slices 0..3, each slice's products under the next slice's reads; the
+    // deferred stores after the first row of products, then the step's loads
+    // (step gg + 1), two per row of products in slices 0 and 1
 #pragma unroll
-    for (int hh = 0; hh < 2; ++hh) {
+    for (int ks = 0; ks < 4; ++ks) {
+      if (ks < 3) read_slice(st, ks + 1);
 #pragma unroll
-      for (int i = 2 * hh; i < 2 * hh + 2; ++i)
+      for (int i = 0; i < TM; ++i) {
 #pragma unroll
-        for (int j = 0; j < TN; ++j) mfma(1, i, j, false);
-      if constexpr (DEFER) {
-        if (hh == 0) {
+        for (int j = 0; j < TN; ++j) mfma(ks, i, j, fresh && ks == 0);
+        if constexpr (DEFER) {
+          if (ks == 0 && i == 0) {
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int h2 = 0; h2 < kStoresPerStep; ++h2) {
+              if constexpr (blk0)
+                store_piece(sp[h2], 2 * u + h2, 0);
+              else
+                store_piece(ob[0][2 * u + h2], 2 * u + h2, sb);
+            }
+          }
+        }
+        if (ks < 2) {
           __builtin_amdgcn_sched_barrier(0);
-          if constexpr (blk0)
-            store_piece(sp, u, 0);
-          else
-            store_piece(ob[0][u], u, sb);
+          load_part(4 * ks + i);
           __builtin_amdgcn_sched_barrier(0);
         }
       }
     }
+    load_advance();
   };
 
-  // ---- prologue: steps 0..2 in flight (each followed by two placeholder
-  // stores with DEFER), slice 0 of step 0 read ----
+  // ---- prologue: step 0 in flight ----
+  load_prep(0);
 #pragma unroll
-  for (int pstep = 0; pstep < kStages - 1; ++pstep) {
-    load_prep(pstep);
-#pragma unroll
-    for (int j = 0; j < kDmaPerTile; ++j) load_part(j);
-    load_advance();
-    if constexpr (DEFER) store_piece(ob[0][0], 0, TM);  // placeholder
-  }
-  wait_vm<2 * (2 * kDmaPerTile + (DEFER ? 2 * kStoresPerStep : 0))>();
-  step_sync();
-  read_slice(0, 0);
+  for (int j = 0; j < kDmaPerTile; ++j) load_part(j);
+  load_advance();
 
   int g = 0;  // the step being multiplied
   for (int L = blockIdx.x; L < tiles; L += gridDim.x) {
     int m0, n0;
     tile_of(L, m0, n0);
     if constexpr (DEFER) {
-      // the first block of eight steps, its first step accumulating onto zero
+      // the first block of four steps, its first step accumulating onto zero
       step(g, std::integral_constant<int, 0>{}, 0, std::true_type{}, std::true_type{});
-      unrolled(std::make_integer_sequence<int, 7>{}, [&](auto v_c) {
+      unrolled(std::make_integer_sequence<int, 3>{}, [&](auto v_c) {
         step(g + decltype(v_c)::value + 1, std::integral_constant<int, decltype(v_c)::value + 1>{}, 0,
              std::false_type{}, std::true_type{});
       });
-      g += 8;
-      for (int s = 8, sb = 1; s < nk; s += 8, ++sb) {
-        unrolled(std::make_integer_sequence<int, 8>{},
+      g += 4;
+      for (int s = 4, sb = 1; s < nk; s += 4, ++sb) {
+        unrolled(std::make_integer_sequence<int, 4>{},
                  [&](auto u_c) { step(g + decltype(u_c)::value, u_c, sb, std::false_type{}, std::false_type{}); });
-        g += 8;
+        g += 4;
 #pragma unroll
         for (int i = 0; i + 2 < TM; ++i)  // the next token block's pieces
 #pragma unroll
