@@ -45,11 +45,12 @@ constexpr int kLdsBytes = kStages * kStageBytes + kSpareBytes;
 constexpr int kDmaPerTile = kTileBytes / (kProjThreads * 16);
 
 // Byte offset of 16-byte chunk `c` of row `r` in a tile (128-byte rows, eight
-// chunks).  The chunks are XOR-swizzled by r % 8: a 16-byte operand read
-// serves 16 lanes (16 consecutive rows) from 64 banks (256 bytes, two rows),
-// and the swizzle gives the even rows, and the odd rows, of each group of
-// eight different chunks.
-__device__ __forceinline__ int tile_off(int r, int c) { return r * kRowBytes + ((c ^ (r & 7)) << 4); }
+// chunks).  A 16-byte operand read serves 16 lanes (16 consecutive rows) from
+// 64 banks (256 bytes: the even rows' chunks in one half, the odd rows' in
+// the other), so the eight even (odd) rows of 16 need eight different chunk
+// positions: the chunks are XOR-swizzled by (r / 2) % 8.  (Swizzled by r % 8,
+// rows r and r + 8 collided, and 49% of the LDS cycles were conflicts.)
+__device__ __forceinline__ int tile_off(int r, int c) { return r * kRowBytes + ((c ^ ((r >> 1) & 7)) << 4); }
 
 // A buffer resource over `bytes` bytes from `base`, as four scalar registers
 // for the assembly loads below (the same descriptor as make_rsrc).
@@ -265,14 +266,16 @@ proj_kernel(LayerPlan P, const uint16_t* __restrict__ xt, const uint16_t* __rest
   // ---- the load stream ----
   // Load j of a wave covers tile rows 8 (kDmaPerTile wave + j) .. + 7: lane
   // l writes row (l / 8), stored chunk l % 8, which holds source chunk
-  // (l % 8) ^ (row % 8) (the swizzle of tile_off).  The offsets within the
+  // (l % 8) ^ (row / 2 % 8) (the swizzle of tile_off), i.e. (l % 8) ^
+  // ((l / 16 + 4 (j % 2)) % 8): two lane offsets, by the parity of j.  The offsets within the
   // tile are the same for Xt and Wp; the tile's first row and the K step go
   // into the descriptor, whose extent ends at the last token (feature), so
   // rows past it read zeros.
   // the lane's part of the offsets (row lane / 8, its source chunk); each
   // load adds its first row through an opaque row pitch, so that the eight
   // sums are formed at the loads rather than held in registers
-  const uint32_t lbase = (uint32_t)(((lane >> 3) * K + 8 * ((lane & 7) ^ ((lane >> 3) & 7))) * 2);
+  const uint32_t lbase0 = (uint32_t)(((lane >> 3) * K + 8 * ((lane & 7) ^ ((lane >> 4) & 7))) * 2);
+  const uint32_t lbase1 = (uint32_t)(((lane >> 3) * K + 8 * ((lane & 7) ^ (((lane >> 4) + 4) & 7))) * 2);
   int dL = blockIdx.x, ds = 0, dm0 = 0, dn0 = 0;  // the next step to load
   if (dL < tiles) tile_of(dL, dm0, dn0);
   // the LDS byte address of the ring (wave-uniform)
@@ -292,7 +295,7 @@ proj_kernel(LayerPlan P, const uint16_t* __restrict__ xt, const uint16_t* __rest
   auto load_part = [&](int j) {
     int pitch = 2 * K;
     asm volatile("" : "+s"(pitch));
-    const uint32_t off = lbase + (uint32_t)(8 * (kDmaPerTile * wave + j) * pitch);
+    const uint32_t off = ((j & 1) ? lbase1 : lbase0) + (uint32_t)(8 * (kDmaPerTile * wave + j) * pitch);
     dma16(lrx, lst + 1024 * j, off);
     dma16(lrw, lst + kTileBytes + 1024 * j, off);
   };
