@@ -142,14 +142,25 @@ conv_x_kernel(LayerPlan P, const uint16_t* __restrict__ x, const float* __restri
   const int K = P.d_model, M = P.tokens;
   if (t0 >= M || c0 >= K) return;  // no barrier follows
   const __amdgpu_buffer_rsrc_t rx = make_rsrc(x, (uint32_t)((int64_t)M * K * 2));
+  // taps: one 16-byte load per channel at W = 4, else one load per tap (an
+  // out-of-range offset, read as zero, for the taps before the first)
+  const __amdgpu_buffer_rsrc_t rw = make_rsrc(conv_x, (uint32_t)(K * P.W * 4));
   float w[8][4];
 #pragma unroll
-  for (int j = 0; j < 8; ++j)
+  for (int j = 0; j < 8; ++j) {
+    const uint32_t row = (uint32_t)((c0 + j) * P.W) * 4u;
+    if (P.W == 4) {
+      const u32x4_t t4 = __builtin_amdgcn_raw_buffer_load_b128(rw, row, 0, 0);
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      const int ti = t - (4 - P.W);
-      w[j][t] = ti >= 0 ? conv_x[(size_t)(c0 + j) * P.W + ti] : 0.0f;
+      for (int t = 0; t < 4; ++t) w[j][t] = __uint_as_float(t4[t]);
+    } else {
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const int ti = t - (4 - P.W);
+        w[j][t] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rw, ti >= 0 ? row + 4u * ti : kOutOfRange, 0, 0));
+      }
     }
+  }
   u32x4_t raw[kConvRun + 3];
 #pragma unroll
   for (int u = 0; u < kConvRun + 3; ++u)
