@@ -532,6 +532,44 @@ combine_kernel(Plan P, const int32_t* __restrict__ cu, const float* __restrict__
 
   const size_t sh = (size_t)s * P.heads + h;
   unsigned char* fr = frags ? frags + sh * P.frag_bytes : nullptr;
+  // bf16 fragments of a slice of S alone: the slice holds R whole rows c of S
+  // (all D columns), so one lane can write the G <= 8 consecutive values j
+  // of a fragment slot at once, through LDS, instead of one 2-byte store per
+  // element (an L2 request each).
+  constexpr int R = E * kThreads / D, G = R < 8 ? R : 8;
+  if constexpr (sizeof(T) == 2 && R >= 2 && R % G == 0 && 8 % G == 0) {
+    if (fr && (blockIdx.y + 1) * E * kThreads <= D * D) {  // uniform
+      __shared__ float tr[E * kThreads];
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        const int x = (blockIdx.y * E + e) * kThreads + tid;
+        const float val = v[e] * invZ;
+        if (S_out) S_out[sh * D * D + x] = val;
+        tr[e * kThreads + tid] = val;
+      }
+      __syncthreads();
+      const int c0 = blockIdx.y * R;  // the slice's first row of S
+      for (int it = tid; it < D * (R / G); it += kThreads) {
+        const int ee = it % D, g = it / D, c = c0 + g * G;
+        const int kb = c / 32, gq = (c % 32) / 8, j0 = c % 8;
+        const int mb = 2 * (ee / 32) + (ee % 8) / 4, m = 4 * ((ee % 32) / 8) + ee % 4;
+        const size_t slot = ((size_t)mb * FragCfg<D>::kNKB + kb) * 64 + 16 * gq + m;
+        uint32_t w[G / 2];
+#pragma unroll
+        for (int i = 0; i < G / 2; ++i)
+          w[i] = pack_bf16x2(tr[(g * G + 2 * i) * D + ee], tr[(g * G + 2 * i + 1) * D + ee]);
+        unsigned char* dst = fr + (slot * 8 + j0) * 2;
+        if constexpr (G == 8) {
+          *reinterpret_cast<u32x4_t*>(dst) = u32x4_t{w[0], w[1], w[2], w[3]};
+        } else if constexpr (G == 4) {
+          *reinterpret_cast<u32x2_t*>(dst) = u32x2_t{w[0], w[1]};
+        } else {
+          *reinterpret_cast<uint32_t*>(dst) = w[0];
+        }
+      }
+      return;
+    }
+  }
 #pragma unroll
   for (int e = 0; e < E; ++e) {
     const int x = (blockIdx.y * E + e) * kThreads + tid;
