@@ -865,8 +865,9 @@ struct ConvRun {
   }
 };
 
-// One element per thread while the grid stays small; four once there are
-// many (sequence, head) pairs.  The result does not depend on the choice.
+// One element per thread while the grid stays small, four or sixteen once
+// there are many (sequence, head) pairs (fewer workgroups, each with more
+// loads in flight).  The result does not depend on the choice.
 template <typename T, int D>
 gbla_status run_combine(const Plan& p, const int32_t* cu, const float* partials, float* S,
                         float* z, unsigned char* frags, float* mz, hipStream_t st) {
@@ -876,9 +877,13 @@ gbla_status run_combine(const Plan& p, const int32_t* cu, const float* partials,
   if (pairs * slices1 <= 4096) {
     hipLaunchKernelGGL((combine_kernel<T, D, 1>), dim3(pairs, slices1), dim3(kThreads), 0, st, p,
                        cu, partials, S, z, frags, mz);
-  } else {
+  } else if (pairs * ((kElems + 4 * kThreads - 1) / (4 * kThreads)) <= 4096) {
     const int slices4 = (kElems + 4 * kThreads - 1) / (4 * kThreads);
     hipLaunchKernelGGL((combine_kernel<T, D, 4>), dim3(pairs, slices4), dim3(kThreads), 0, st, p,
+                       cu, partials, S, z, frags, mz);
+  } else {
+    const int slices16 = (kElems + 16 * kThreads - 1) / (16 * kThreads);
+    hipLaunchKernelGGL((combine_kernel<T, D, 16>), dim3(pairs, slices16), dim3(kThreads), 0, st, p,
                        cu, partials, S, z, frags, mz);
   }
   return last_launch_status();
