@@ -155,6 +155,93 @@ __device__ __forceinline__ void wait_vm() {
 // the compiler from moving LDS accesses across the barrier.
 __device__ __forceinline__ void ring_sync() { asm volatile("s_barrier" ::: "memory"); }
 
+// Ragged batches are reduced longest unit first: lengths follow a wide
+// distribution, and with one workgroup per CU the grid otherwise ends on a
+// tail of long chunks that started last.  Rank r of a head takes, in order,
+// every full chunk (sequence order), then the last, partial chunk of each
+// sequence (an empty sequence counts as one of zero tokens) by its number of
+// 32-token steps, most first, ties in sequence order.  Every thread of the
+// block calls these helpers.
+
+// The n-th unit in sequence order, where sequence s owns cnt(s) units:
+// sets *s_out and *idx_out and returns true, or returns false and sets
+// *total to the number of units when n is past them.
+template <int NT, typename Cnt>
+__device__ __forceinline__ bool locate_by(int nseq, int n, Cnt cnt, int* red, int* s_out,
+                                          int* idx_out, int* total) {
+  __shared__ int found[2];
+  if (threadIdx.x == 0) found[0] = -1;
+  int running = 0;
+  for (int base = 0; base < nseq; base += NT) {
+    const int sq = base + (int)threadIdx.x;
+    const int c = sq < nseq ? cnt(sq) : 0;
+    int all;
+    const int incl = block_incl_scan<NT>(c, red, &all);
+    if (sq < nseq && n >= running + incl - c && n < running + incl) {
+      found[0] = sq;
+      found[1] = n - running - (incl - c);
+    }
+    __syncthreads();
+    if (found[0] >= 0) break;
+    running += all;
+  }
+  *s_out = found[0];
+  *idx_out = found[1];
+  *total = running;
+  __syncthreads();  // found[] is reused by the next call
+  return *s_out >= 0;
+}
+
+// Rank r -> (sequence, chunk index, record slot units_before(s) + chunk).
+template <int NT>
+__device__ __forceinline__ bool lpt_unit(const int32_t* cu, int nseq, int unit, int r, int* s_out,
+                                         int* idx_out, int* slot_out) {
+  constexpr int kBuckets = S128::kMaxChunk / S128::kStep + 1;
+  __shared__ int red[NT / 64];
+  __shared__ int hist[kBuckets];
+  __shared__ int pick[2];
+  auto len = [&](int sq) { return (int64_t)cu[sq + 1] - cu[sq]; };
+  auto full = [&](int sq) { return (int)(len(sq) / unit); };
+  auto partial = [&](int sq) { const int64_t n = len(sq); return n == 0 || n % unit != 0; };
+  auto bucket = [&](int sq) { return (int)((len(sq) % unit + S128::kStep - 1) / S128::kStep); };
+  int s, idx, nfull;
+  if (!locate_by<NT>(nseq, r, full, red, &s, &idx, &nfull)) {
+    for (int b = threadIdx.x; b < kBuckets; b += NT) hist[b] = 0;
+    __syncthreads();
+    for (int sq = threadIdx.x; sq < nseq; sq += NT)
+      if (partial(sq)) atomicAdd(&hist[bucket(sq)], 1);
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      int q = r - nfull;
+      pick[0] = -1;
+      for (int b = kBuckets - 1; b >= 0; --b) {
+        if (q < hist[b]) {
+          pick[0] = b;
+          pick[1] = q;
+          break;
+        }
+        q -= hist[b];
+      }
+    }
+    __syncthreads();
+    const int pb = pick[0], pq = pick[1];
+    if (pb < 0) return false;  // past the last unit of the head
+    int in_bucket, unused;
+    if (!locate_by<NT>(nseq, pq, [&](int sq) { return partial(sq) && bucket(sq) == pb ? 1 : 0; },
+                       red, &s, &in_bucket, &unused))
+      return false;  // not reached: the histogram counted this unit
+    idx = full(s);
+  }
+  int before = 0;
+  for (int sq = threadIdx.x; sq < s; sq += NT) before += units_of(len(sq), unit);
+  int all;
+  (void)block_incl_scan<NT>(before, red, &all);
+  *s_out = s;
+  *idx_out = idx;
+  *slot_out = all + idx;
+  return true;
+}
+
 __global__ void __launch_bounds__(S128::kNT, 1)
 state128_kernel(Plan P, const uint16_t* __restrict__ kin, const uint16_t* __restrict__ vin,
                 const uint16_t* __restrict__ ain, const float* __restrict__ conv_w,
@@ -163,11 +250,19 @@ state128_kernel(Plan P, const uint16_t* __restrict__ kin, const uint16_t* __rest
   constexpr int D = C::D;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int h = blockIdx.y, g = blockIdx.x;
-  int s, chunk;
-  if (!unit_of<C::kNT>(P, cu, P.chunk, P.chunks_per_seq, g, &s, &chunk)) return;
+  // dense: grid (units, heads) in sequence order; ragged: one dimension,
+  // heads innermost, longest unit first
+  const int h = P.ragged ? (int)(blockIdx.x % P.heads) : (int)blockIdx.y;
+  int s, chunk, g;
+  if (P.ragged) {
+    if (!lpt_unit<C::kNT>(cu, P.nseq, P.chunk, (int)(blockIdx.x / P.heads), &s, &chunk, &g)) return;
+  } else {
+    g = blockIdx.x;
+    if (!unit_of<C::kNT>(P, cu, P.chunk, P.chunks_per_seq, g, &s, &chunk)) return;
+  }
   s = __builtin_amdgcn_readfirstlane(s);
   chunk = __builtin_amdgcn_readfirstlane(chunk);
+  g = __builtin_amdgcn_readfirstlane(g);
   int64_t len, base_row;
   seq_geometry(P, cu, s, h, &len, &base_row);
   const int64_t t0 = (int64_t)chunk * P.chunk;
@@ -514,7 +609,7 @@ gbla_status launch_state128(const Plan& p, const void* k, const void* v, const v
                             const float* conv_w, const int32_t* cu, float* partials, hipStream_t st) {
   if (p.d != S128::D || p.chunk > S128::kMaxChunk || p.chunk % S128::kStep != 0)
     return GBLA_ERR_UNSUPPORTED;  // the plan never asks for this
-  const dim3 grid(p.units, p.heads);
+  const dim3 grid = p.ragged ? dim3((unsigned)p.units * (unsigned)p.heads) : dim3(p.units, p.heads);
   hipLaunchKernelGGL(state128_kernel, grid, dim3(S128::kNT), 0, st, p, (const uint16_t*)k,
                      (const uint16_t*)v, (const uint16_t*)a, conv_w, cu, partials);
   return hipGetLastError() == hipSuccess ? GBLA_OK : GBLA_ERR_HIP;
