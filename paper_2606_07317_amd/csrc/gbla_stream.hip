@@ -466,7 +466,18 @@ readout_stream_kernel(Plan P, const uint16_t* __restrict__ qin, const uint16_t* 
   __shared__ __attribute__((aligned(16))) float gam[D];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int h = blockIdx.y, g = blockIdx.x;
+  // At d = 128 a (sequence, head) reads 37 KB of operands, and each XCD
+  // has its own L2: workgroups go to the eight XCDs in turn by linear id, so
+  // XCD x is given one contiguous run of tiles (v below is a bijection of
+  // the grid) and fetches a pair's operands once instead of all eight XCDs.
+  int h = blockIdx.y, g = blockIdx.x;
+  if constexpr (D == 128) {
+    const int n = (int)(gridDim.x * gridDim.y), L = (int)(blockIdx.x + blockIdx.y * gridDim.x);
+    const int q = n >> 3, r = n & 7, x = L & 7;
+    const int v = x * q + min(x, r) + (L >> 3);
+    g = v % (int)gridDim.x;
+    h = v / (int)gridDim.x;
+  }
   int s, tile;
   if (!unit_of(P, cu, P.rtile, P.rtiles_per_seq, g, &s, &tile)) return;
   s = __builtin_amdgcn_readfirstlane(s);
