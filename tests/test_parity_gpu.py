@@ -77,6 +77,11 @@ SMALL_CASES = {
 RAGGED_CASES = {
     "ragged_d128_mixed": (small("ragged64_d128", heads=2, seed=31), [5, 0, 300, 1, 77, 2049, 3]),
     "ragged_d64_long": (small("ragged64_d128", heads=3, head_dim=64, seed=32), [4100, 17, 0, 0, 999]),
+    # 256-token chunks at this size: whole-chunk sequences (no partial unit),
+    # partial units that tie on their number of 32-token steps, an empty and a
+    # one-token sequence (the d = 128 state pass takes units longest first)
+    "ragged_d128_units": (small("ragged64_d128", heads=2, seed=34),
+                          [512, 256, 1, 768, 300, 0, 256, 33, 32, 1024, 255]),
     "ragged_f32_d32": (inputs.Workload("rf32", batch=3, heads=2, seqlen=0, head_dim=32, conv_width=4,
                                        dtype=inputs.F32, seed=33, ragged=True), [31, 2, 600]),
 }
